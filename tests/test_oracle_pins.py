@@ -1,0 +1,418 @@
+"""CPU pins of the float64 oracle against closed forms, invariants the paper
+fixes, and brute force on tiny inputs.  None of these re-calls the oracle's own
+formula to check itself: each compares it with something computed another way
+(scalar loops, complex arithmetic, erf, permutations, full-sequence masks)."""
+import cmath
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+from workloads import BlockShape, WORKLOADS, draw_block_weights, draw_time_weights, make_rng
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TINY = BlockShape(dim=32, n_heads=2, head_dim=16, ffn_dim=64, frames=2, lat_h=2, lat_w=2)
+
+
+def _tiny_weights(seed=0, shape=TINY):
+    rng = np.random.default_rng(seed)
+    w = draw_block_weights(make_rng(90 + seed), shape)
+    # larger spread than the workloads so every branch carries visible signal
+    for k in w:
+        if k.startswith("w_"):
+            w[k] = rng.standard_normal(w[k].shape) * 0.3
+    tw = draw_time_weights(make_rng(95 + seed), shape.dim, 16)
+    return w, tw
+
+
+# --------------------------------------------------------------------------
+# brute force: scalar loops with math / cmath on tiny shapes
+# --------------------------------------------------------------------------
+def _bf_linear(x, W, b):
+    return [sum(W[o][i] * x[i] for i in range(len(x))) + b[o] for o in range(len(W))]
+
+
+def _bf_rms(z, eps, g=None):
+    ms = sum(v * v for v in z) / len(z)
+    r = 1.0 / math.sqrt(ms + eps)
+    return [z[i] * r * (1.0 if g is None else g[i]) for i in range(len(z))]
+
+
+def _bf_rope_head(vec, pos, theta):
+    d = len(vec)
+    dh = 2 * (d // 6)
+    segs = [d - 2 * dh, dh, dh]
+    out = list(vec)
+    start = 0
+    for axis, seg in enumerate(segs):
+        for k in range(seg // 2):
+            ang = pos[axis] * theta ** (-2.0 * k / seg)
+            zc = complex(vec[start + 2 * k], vec[start + 2 * k + 1]) * cmath.exp(1j * ang)
+            out[start + 2 * k] = zc.real
+            out[start + 2 * k + 1] = zc.imag
+        start += seg
+    return out
+
+
+def _bf_attn_row(q, K, V):
+    d = len(q)
+    s = [sum(q[i] * k[i] for i in range(d)) / math.sqrt(d) for k in K]
+    mx = max(s)
+    e = [math.exp(v - mx) for v in s]
+    tot = sum(e)
+    return [sum(e[j] * V[j][i] for j in range(len(K))) / tot for i in range(d)]
+
+
+def _bf_gelu(y):
+    return 0.5 * y * (1.0 + math.tanh(math.sqrt(2.0 / math.pi) * (y + 0.044715 * y ** 3)))
+
+
+def _bf_block(x, cache_k, cache_v, pos0, m_t, ctxk, ctxv, w, sh):
+    D, H, d = sh.dim, sh.n_heads, sh.head_dim
+    Mt = [[float(m_t[r][i]) + float(w["mod_table"][r][i]) for i in range(D)] for r in range(6)]
+    W = {k: np.asarray(v).tolist() for k, v in w.items()}
+    L = len(x)
+    qs, ks, vs = [], [], []
+    for n in range(L):
+        f, rem = divmod(n, sh.lat_h * sh.lat_w)
+        i, j = divmod(rem, sh.lat_w)
+        pos = (pos0 + f, i, j)
+        h1 = [v * (1 + Mt[1][c]) + Mt[0][c] for c, v in enumerate(_bf_rms(list(x[n]), sh.eps))]
+        qkv = _bf_linear(h1, W["w_qkv"], W["b_qkv"])
+        qn = _bf_rms(qkv[:D], sh.eps, W["g_q"])
+        kn = _bf_rms(qkv[D:2 * D], sh.eps, W["g_k"])
+        qs.append([_bf_rope_head(qn[h * d:(h + 1) * d], pos, sh.theta) for h in range(H)])
+        ks.append([_bf_rope_head(kn[h * d:(h + 1) * d], pos, sh.theta) for h in range(H)])
+        vs.append([qkv[2 * D + h * d:2 * D + (h + 1) * d] for h in range(H)])
+    Kall = [list(map(list, np.asarray(cache_k)[c])) for c in range(len(cache_k))] + ks
+    Vall = [list(map(list, np.asarray(cache_v)[c])) for c in range(len(cache_v))] + vs
+    outs = []
+    for n in range(L):
+        o = []
+        for h in range(H):
+            o += _bf_attn_row(qs[n][h], [kk[h] for kk in Kall], [vv[h] for vv in Vall])
+        y = _bf_linear(o, W["w_o"], W["b_o"])
+        x1 = [x[n][c] + Mt[2][c] * y[c] for c in range(D)]
+        h3 = _bf_rms(x1, sh.eps, W["g_n3"])
+        qc = _bf_rms(_bf_linear(h3, W["w_cq"], W["b_cq"]), sh.eps, W["g_cq"])
+        oc = []
+        for h in range(H):
+            oc += _bf_attn_row(qc[h * d:(h + 1) * d], [list(r[h * d:(h + 1) * d]) for r in ctxk],
+                               [list(r[h * d:(h + 1) * d]) for r in ctxv])
+        yc = _bf_linear(oc, W["w_co"], W["b_co"])
+        x2 = [x1[c] + yc[c] for c in range(D)]
+        h2 = [v * (1 + Mt[4][c]) + Mt[3][c] for c, v in enumerate(_bf_rms(x2, sh.eps))]
+        u = [_bf_gelu(v) for v in _bf_linear(h2, W["w_1"], W["b_1"])]
+        y2 = _bf_linear(u, W["w_2"], W["b_2"])
+        outs.append([x2[c] + Mt[5][c] * y2[c] for c in range(D)])
+    return np.array(outs), np.array(ks), np.array(vs)
+
+
+@pytest.mark.parametrize("cache_chunks", [0, 1, 2])
+def test_block_matches_brute_force(cache_chunks):
+    sh = TINY
+    w, tw = _tiny_weights(cache_chunks)
+    rng = np.random.default_rng(7 + cache_chunks)
+    c = cache_chunks * sh.chunk_tokens
+    x = rng.standard_normal((sh.chunk_tokens, sh.dim))
+    ck = rng.standard_normal((c, sh.n_heads, sh.head_dim))
+    cv = rng.standard_normal((c, sh.n_heads, sh.head_dim))
+    ctx = rng.standard_normal((3, sh.dim))
+    m_t = O.time_modulation(500.0, tw, sh.dim)
+    kc, vc = O.context_kv(ctx, w, sh.eps)
+    pos0 = 2 * cache_chunks + 1
+    ref = O.block_forward(x, ck, cv, pos0, m_t, kc, vc, w, sh)
+    bf_out, bf_k, bf_v = _bf_block(x, ck, cv, pos0, m_t, kc.tolist(), vc.tolist(), w, sh)
+    np.testing.assert_allclose(ref["out"], bf_out, rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(ref["k_new"], bf_k, rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(ref["v_new"], bf_v, rtol=1e-11, atol=1e-11)
+    # the branches carry signal: the test is not vacuous
+    assert np.abs(ref["out"] - x).max() > 1e-2
+
+
+def test_context_kv_brute_force():
+    w, _ = _tiny_weights(3)
+    ctx = np.random.default_rng(3).standard_normal((5, TINY.dim))
+    kc, vc = O.context_kv(ctx, w, TINY.eps)
+    W = {k: np.asarray(v).tolist() for k, v in w.items()}
+    for r in range(5):
+        k_bf = _bf_rms(_bf_linear(list(ctx[r]), W["w_ck"], W["b_ck"]), TINY.eps, W["g_ck"])
+        v_bf = _bf_linear(list(ctx[r]), W["w_cv"], W["b_cv"])
+        np.testing.assert_allclose(kc[r], k_bf, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(vc[r], v_bf, rtol=1e-12, atol=1e-12)
+
+
+def test_time_modulation_brute_force():
+    _, tw = _tiny_weights(4)
+    D = TINY.dim
+    t = 750.0
+    s = [math.cos(t * 10000.0 ** (-k / 8)) for k in range(8)] + \
+        [math.sin(t * 10000.0 ** (-k / 8)) for k in range(8)]
+    W = {k: np.asarray(v).tolist() for k, v in tw.items()}
+    silu = lambda z: z / (1.0 + math.exp(-z))  # noqa: E731
+    e = _bf_linear([silu(v) for v in _bf_linear(s, W["w_t1"], W["b_t1"])], W["w_t2"], W["b_t2"])
+    m = _bf_linear([silu(v) for v in e], W["w_m"], W["b_m"])
+    np.testing.assert_allclose(O.time_modulation(t, tw, D).ravel(), m, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# invariants the paper fixes: chunk-wise generation over a KV cache
+# --------------------------------------------------------------------------
+def _chain(seed=11, C=3, window=None):
+    sh = TINY
+    w, tw = _tiny_weights(seed)
+    rng = np.random.default_rng(seed)
+    xs = [rng.standard_normal((sh.chunk_tokens, sh.dim)) for _ in range(C)]
+    m_ts = [O.time_modulation(t, tw, sh.dim) for t in (1000.0, 750.0, 250.0)[:C]]
+    ctx = rng.standard_normal((4, sh.dim))
+    kc, vc = O.context_kv(ctx, w, sh.eps)
+    full = O.full_sequence_forward(xs, m_ts, 5, kc, vc, w, sh, window=window)
+    return sh, w, xs, m_ts, kc, vc, full
+
+
+@pytest.mark.parametrize("chunk", [0, 1, 2])
+def test_chunk_with_cache_equals_full_sequence(chunk):
+    sh, w, xs, m_ts, kc, vc, full = _chain()
+    L = sh.chunk_tokens
+    ck, cv = full["k"][:chunk * L], full["v"][:chunk * L]
+    res = O.block_forward(xs[chunk], ck, cv, 5 + chunk * sh.frames, m_ts[chunk], kc, vc, w, sh)
+    sl = slice(chunk * L, (chunk + 1) * L)
+    for key in ("out", "x1", "x2", "o"):
+        np.testing.assert_allclose(res[key], full[key][sl], rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(res["k_new"], full["k"][sl], rtol=1e-12, atol=1e-12)
+
+
+def test_window_of_earlier_chunks():
+    """With a window of W earlier chunks, the chunk sees exactly the last W chunks."""
+    sh, w, xs, m_ts, kc, vc, full = _chain(window=1)
+    L = sh.chunk_tokens
+    res = O.block_forward(xs[2], full["k"][L:2 * L], full["v"][L:2 * L], 5 + 2 * sh.frames,
+                          m_ts[2], kc, vc, w, sh)
+    np.testing.assert_allclose(res["out"], full["out"][2 * L:], rtol=1e-11, atol=1e-11)
+    _, _, _, _, _, _, full_nowin = _chain(window=None)
+    assert np.abs(full_nowin["out"][2 * L:] - full["out"][2 * L:]).max() > 1e-6
+
+
+def test_later_chunks_do_not_change_earlier_rows():
+    sh, w, xs, m_ts, kc, vc, full = _chain()
+    xs2 = [a.copy() for a in xs]
+    xs2[2] = xs2[2] + 3.0 * np.random.default_rng(5).standard_normal(xs2[2].shape)
+    full2 = O.full_sequence_forward(xs2, m_ts, 5, kc, vc, w, sh)
+    L = sh.chunk_tokens
+    for key in ("out", "o", "x1", "x2"):
+        assert np.array_equal(full[key][:2 * L], full2[key][:2 * L]), key
+        assert not np.array_equal(full[key][2 * L:], full2[key][2 * L:]), key
+
+
+# --------------------------------------------------------------------------
+# attention closed forms
+# --------------------------------------------------------------------------
+def test_softmax_rows_sum_to_one_long_cache():
+    rng = np.random.default_rng(1)
+    q = rng.standard_normal((64, 1, 128))
+    k = rng.standard_normal((37440, 1, 128)) * 3.0
+    v = rng.standard_normal((37440, 1, 128))
+    _, p = O.attention(q, k, v, return_probs=True)
+    np.testing.assert_allclose(p.sum(axis=-1), 1.0, atol=1e-12, rtol=0)
+    assert (p >= 0).all()
+
+
+def test_attention_zero_query_is_mean_of_values():
+    rng = np.random.default_rng(2)
+    v = rng.standard_normal((37, 3, 16))
+    o = O.attention(np.zeros((5, 3, 16)), rng.standard_normal((37, 3, 16)), v)
+    np.testing.assert_allclose(o, np.broadcast_to(v.mean(axis=0), o.shape), rtol=1e-13, atol=1e-13)
+
+
+def test_attention_single_key_returns_its_value():
+    rng = np.random.default_rng(3)
+    v = rng.standard_normal((1, 2, 8))
+    o = O.attention(rng.standard_normal((6, 2, 8)), rng.standard_normal((1, 2, 8)), v)
+    assert np.array_equal(o, np.broadcast_to(v[0], o.shape))
+
+
+def test_attention_key_permutation_invariance():
+    rng = np.random.default_rng(4)
+    q, k, v = (rng.standard_normal((9, 2, 16)) for _ in range(3))
+    k = np.concatenate([k, rng.standard_normal((40, 2, 16))])
+    v = np.concatenate([v, rng.standard_normal((40, 2, 16))])
+    perm = rng.permutation(k.shape[0])
+    np.testing.assert_allclose(O.attention(q, k, v), O.attention(q, k[perm], v[perm]),
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_attention_dominant_key_selects_its_value():
+    rng = np.random.default_rng(6)
+    d = 16
+    k = rng.standard_normal((20, 1, d))
+    v = rng.standard_normal((20, 1, d))
+    q = (k[7:8] * 200.0)
+    o = O.attention(q, k, v)
+    np.testing.assert_allclose(o[0, 0], v[7, 0], atol=1e-9)
+
+
+def test_attention_scale_is_inverse_sqrt_head_dim():
+    # two keys with score gap g: weights are sigmoid(+-g / sqrt(d))
+    d = 64
+    q = np.zeros((1, 1, d)); q[0, 0, 0] = 1.0
+    k = np.zeros((2, 1, d)); k[0, 0, 0] = 8.0
+    v = np.zeros((2, 1, d)); v[0, 0, 1] = 1.0; v[1, 0, 2] = 1.0
+    o = O.attention(q, k, v)
+    p0 = 1.0 / (1.0 + math.exp(-8.0 / math.sqrt(d)))
+    assert abs(o[0, 0, 1] - p0) < 1e-14 and abs(o[0, 0, 2] - (1 - p0)) < 1e-14
+
+
+def test_cross_attention_single_text_token():
+    sh = TINY
+    w, tw = _tiny_weights(8)
+    rng = np.random.default_rng(8)
+    kc, vc = O.context_kv(rng.standard_normal((1, sh.dim)), w, sh.eps)
+    res = O.block_forward(rng.standard_normal((sh.chunk_tokens, sh.dim)),
+                          np.zeros((0, 2, 16)), np.zeros((0, 2, 16)), 0,
+                          O.time_modulation(250.0, tw, sh.dim), kc, vc, w, sh)
+    assert np.array_equal(res["oc"], np.broadcast_to(vc[0], res["oc"].shape))
+
+
+# --------------------------------------------------------------------------
+# RoPE
+# --------------------------------------------------------------------------
+def test_rope_split_values():
+    assert O.rope_split(128) == (44, 42, 42)
+    assert O.rope_split(64) == (24, 20, 20)
+    assert sum(O.rope_split(16)) == 16
+
+
+def test_rope_position_zero_is_identity():
+    z = np.random.default_rng(9).standard_normal((4, 3, 64))
+    assert np.array_equal(O.rope3d(z, np.zeros((4, 3), dtype=np.int64), 10000.0), z)
+
+
+def test_rope_is_complex_rotation():
+    rng = np.random.default_rng(10)
+    d = 64
+    z = rng.standard_normal((5, 2, d))
+    pos = rng.integers(0, 40, size=(5, 3))
+    out = O.rope3d(z, pos, 10000.0)
+    start = 0
+    for axis, seg in enumerate(O.rope_split(d)):
+        k = np.arange(seg // 2)
+        ang = pos[:, axis:axis + 1] * (10000.0 ** (-(2.0 * k) / seg))[None, :]
+        zc = (z[:, :, start:start + seg:2] + 1j * z[:, :, start + 1:start + seg:2]) \
+            * np.exp(1j * ang)[:, None, :]
+        np.testing.assert_allclose(out[:, :, start:start + seg:2], zc.real, atol=1e-13)
+        np.testing.assert_allclose(out[:, :, start + 1:start + seg:2], zc.imag, atol=1e-13)
+        start += seg
+    np.testing.assert_allclose(np.linalg.norm(out, axis=-1), np.linalg.norm(z, axis=-1), rtol=1e-13)
+
+
+def test_rope_relative_positions():
+    """Scores depend only on position differences: shifting every temporal
+    position (queries and cached keys) by the same amount leaves them unchanged."""
+    rng = np.random.default_rng(12)
+    q = rng.standard_normal((6, 2, 128))
+    k = rng.standard_normal((9, 2, 128))
+    pq = rng.integers(0, 30, size=(6, 3))
+    pk = rng.integers(0, 30, size=(9, 3))
+    shift = np.array([[17, 0, 0]])
+    s0 = np.einsum("qhd,khd->hqk", O.rope3d(q, pq, 1e4), O.rope3d(k, pk, 1e4))
+    s1 = np.einsum("qhd,khd->hqk", O.rope3d(q, pq + shift, 1e4), O.rope3d(k, pk + shift, 1e4))
+    np.testing.assert_allclose(s0, s1, rtol=1e-10, atol=1e-10)
+    s2 = np.einsum("qhd,khd->hqk", O.rope3d(q, pq + shift, 1e4), O.rope3d(k, pk, 1e4))
+    assert np.abs(s0 - s2).max() > 1e-3
+
+
+def test_chunk_positions_order():
+    pos = O.chunk_positions(3, 2, 4, 10)
+    assert pos.shape == (24, 3)
+    # token n = (f * lat_h + i) * lat_w + j
+    for n in range(24):
+        f, rem = divmod(n, 8)
+        i, j = divmod(rem, 4)
+        assert tuple(pos[n]) == (10 + f, i, j)
+
+
+# --------------------------------------------------------------------------
+# norms, GELU, linear orientation, time embedding, gates
+# --------------------------------------------------------------------------
+def test_rms_norm_scale_invariance_and_unit_rms():
+    z = np.random.default_rng(13).standard_normal((7, 96)) * 5.0
+    y = O.rms_norm(z, 1e-6)
+    # invariant up to eps: relative gap eps / (2 mean(z^2)) ~ 2e-8 here
+    np.testing.assert_allclose(O.rms_norm(37.0 * z, 1e-6), y, rtol=1e-7)
+    np.testing.assert_allclose(O.rms_norm(37.0 * z, 0.0), O.rms_norm(z, 0.0), rtol=1e-14)
+    ms = np.mean(z * z, axis=-1)
+    np.testing.assert_allclose(np.mean(y * y, axis=-1), ms / (ms + 1e-6), rtol=1e-13)
+
+
+def test_gelu_tanh_identities():
+    y = np.linspace(-12, 12, 40001)
+    g = O.gelu_tanh(y)
+    np.testing.assert_allclose(g - O.gelu_tanh(-y), y, rtol=1e-13, atol=1e-13)
+    assert O.gelu_tanh(np.array([0.0]))[0] == 0.0
+    from scipy.special import erf
+    gap = np.abs(g - 0.5 * y * (1.0 + erf(y / math.sqrt(2.0))))
+    assert gap.max() < 5e-4        # the tanh form's known distance to the erf form
+    assert gap.max() > 1e-4        # and it is the tanh form, not the erf one
+
+
+def test_linear_orientation_out_in():
+    W = np.zeros((5, 3)); W[4, 1] = 1.0
+    y = O.linear(np.array([[10.0, 20.0, 30.0]]), W, np.arange(5.0))
+    assert y.tolist() == [[0.0, 1.0, 2.0, 3.0, 24.0]]
+
+
+def test_timestep_sinusoid_closed_form():
+    s0 = O.timestep_sinusoid(0.0)
+    assert s0.tolist() == [1.0] * 128 + [0.0] * 128
+    s = O.timestep_sinusoid(750.0)
+    assert s[0] == math.cos(750.0) and s[128] == math.sin(750.0)
+    assert abs(s[127] - math.cos(750.0 * 10000.0 ** (-127 / 128))) < 1e-12
+
+
+def test_zero_gates_return_input_exactly():
+    sh = TINY
+    w, tw = _tiny_weights(14)
+    m_t = O.time_modulation(1000.0, tw, sh.dim)
+    w = dict(w)
+    w["mod_table"] = w["mod_table"].astype(np.float64).copy()
+    w["mod_table"][2] = -m_t[2]
+    w["mod_table"][5] = -m_t[5]
+    w["w_co"] = np.zeros_like(w["w_co"]); w["b_co"] = np.zeros_like(w["b_co"])
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((sh.chunk_tokens, sh.dim))
+    kc, vc = O.context_kv(rng.standard_normal((3, sh.dim)), w, sh.eps)
+    res = O.block_forward(x, np.zeros((0, 2, 16)), np.zeros((0, 2, 16)), 0, m_t, kc, vc, w, sh)
+    assert np.array_equal(res["out"], x)
+
+
+def test_adaln_zero_modulation_is_plain_rms():
+    sh = TINY
+    w, _ = _tiny_weights(15)
+    w = dict(w)
+    w["mod_table"] = np.zeros((6, sh.dim))
+    x = np.random.default_rng(15).standard_normal((sh.chunk_tokens, sh.dim))
+    # with zero modulation the QKV input is rms(x): check through the value path
+    res = O.block_forward(x, np.zeros((0, 2, 16)), np.zeros((0, 2, 16)), 0,
+                          np.zeros((6, sh.dim)), *O.context_kv(x[:2], w, sh.eps), w, sh)
+    v_expect = O.linear(x / np.sqrt(np.mean(x * x, -1, keepdims=True) + sh.eps),
+                        w["w_qkv"][2 * sh.dim:], w["b_qkv"][2 * sh.dim:])
+    np.testing.assert_allclose(res["v_new"].reshape(-1, sh.dim), v_expect, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# golden: structural numbers the paper prints
+# --------------------------------------------------------------------------
+def test_workloads_respect_paper_settings():
+    with open(os.path.join(GOLDEN, "paper_settings.json")) as f:
+        g = json.load(f)
+    assert g["frames_per_chunk"] == 3 and max(g["kv_window_chunks"]) == 7
+    n_cfg = len(g["denoise_steps"]) * len(g["sparsity"]) * len(g["kv_window_chunks"]) * \
+        len(g["quant_modes"])
+    assert n_cfg == g["n_fidelity_configs"] == 90
+    for wl in WORKLOADS.values():
+        assert wl.shape.frames == g["frames_per_chunk"]
+        assert max(wl.cache_chunks) <= max(g["kv_window_chunks"])
+        assert len(set(wl.timesteps)) <= max(g["denoise_steps"])
