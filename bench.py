@@ -1,0 +1,223 @@
+"""Benchmark: ms per chunk-denoise-step per block on one MI355X.
+
+Workload: the 1.3B-class AR-DiT block (hidden 1536, 12 heads x 128, FFN
+8960), one stream, a 4680-token chunk (3 latent frames of 30 x 52) over a
+28080-token cache (6 earlier chunks), 512 text tokens, 30 layers.  One bench
+step is one denoising step of the chunk: the time modulation for that step's
+timestep (1000/750/500/250 in turn) followed by all 30 blocks through
+ardit_stack_fwd.  value = ms per step / 30.  Inputs are synthetic (seeded
+normal draws on the device), resident in HBM before timing starts.
+
+The JSON line also carries the roofline of the dominant kernel (paged
+self-attention: 4 L_q L_k D flops per launch, timed with HIP events around
+each launch on the stream it runs on) and the float64 CPU oracle timed on
+one block step of layer 0 (cpu_baseline)."""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+LAYERS = 30
+TIMESTEPS = (1000.0, 750.0, 500.0, 250.0)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--layers", type=int, default=LAYERS)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+class Model:
+    """Weights, pages and text K/V of every layer, drawn on the device."""
+
+    def __init__(self, A, sh, n_layers, cache_len, ctx_len, dev):
+        import torch
+        self.A, self.sh, self.n_layers = A, sh, n_layers
+        D, F, H, d = sh.dim, sh.ffn_dim, sh.n_heads, sh.head_dim
+        T = sh.tokens_per_frame
+        self.cache_len, self.ctx_len = cache_len, ctx_len
+        self.frames = cache_len // T + sh.frames
+        self.dims = A.dims_from_shape(sh)
+        self.batch = A.Batch([sh.chunk_tokens], [cache_len], [cache_len // T], [ctx_len])
+        self.ws_bytes = A.ardit_workspace_size(self.dims, self.batch)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+        from workloads.gen import block_weight_shapes, GAIN_NAMES
+        shapes = block_weight_shapes(sh)
+        self.w, self.kv, self.ctx_k, self.ctx_v, self.keep = [], [], [], [], []
+        self.table = torch.arange(self.frames, dtype=torch.int32, device=dev).reshape(1, -1)
+        for layer in range(n_layers):
+            g = torch.Generator(device=dev)
+            g.manual_seed(15319 + 3 + 1000 * layer)
+            wd = {}
+            for name, shp in shapes.items():
+                t = torch.randn(shp, generator=g, device=dev, dtype=torch.float32) * 0.02
+                if name in GAIN_NAMES:
+                    t += 1.0
+                wd[name] = t if name == "mod_table" else t.to(torch.bfloat16)
+            kp = torch.randn((self.frames, H, T, d), generator=g, device=dev).to(torch.bfloat16)
+            vp = torch.randn((self.frames, H, d, T), generator=g, device=dev).to(torch.bfloat16)
+            ctx = torch.randn((ctx_len, D), generator=g, device=dev).to(torch.bfloat16)
+            ck = torch.empty(ctx_len * D, dtype=torch.bfloat16, device=dev)
+            cv = torch.empty_like(ck)
+            w = A.block_weights(wd)
+            A.ardit_ctx_kv(None, self.dims, self.batch, ctx, w, ck, cv, self.ws, self.ws_bytes)
+            self.w.append(w)
+            self.kv.append(A.kv_paged(kp, vp, self.table, self.frames, self.frames))
+            self.ctx_k.append(ck)
+            self.ctx_v.append(cv)
+            self.keep.append((wd, kp, vp, ctx))
+        g = torch.Generator(device=dev)
+        g.manual_seed(15319 + 3)
+        tshapes = {"w_t1": (D, 256), "b_t1": (D,), "w_t2": (D, D), "b_t2": (D,),
+                   "w_m": (6 * D, D), "b_m": (6 * D,)}
+        self.tw_dev = {k: (torch.randn(s, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+                       for k, s in tshapes.items()}
+        self.tw = A.time_weights(self.tw_dev)
+        self.xs = [torch.randn((sh.chunk_tokens, D), generator=g, device=dev).to(torch.bfloat16)
+                   for _ in TIMESTEPS]
+        self.mod = torch.empty((1, 6, D), dtype=torch.float32, device=dev)
+        self.out = torch.empty_like(self.xs[0])
+
+    def step(self, k):
+        A = self.A
+        A.ardit_time_mod(None, self.dims, [TIMESTEPS[k % len(TIMESTEPS)]], self.tw, self.mod,
+                         self.ws, self.ws_bytes)
+        A.ardit_stack_fwd(None, self.dims, self.batch, self.xs[k % len(self.xs)], self.kv,
+                          self.mod, self.ctx_k, self.ctx_v, self.w, self.out, self.ws,
+                          self.ws_bytes)
+
+
+def cpu_baseline(model):
+    """The float64 oracle on one block step (layer 0, step 0) of the same
+    workload, on the host cores, with the layer's own inputs copied back."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+    from workloads import bits_to_f32
+
+    def host(t):
+        if t.dtype == torch.bfloat16:
+            return bits_to_f32(t.view(torch.int16).cpu().numpy().view(np.uint16))
+        return t.float().cpu().numpy()
+
+    sh = model.sh
+    wd, kp, vp, ctx = model.keep[0]
+    w = {k: host(v) for k, v in wd.items()}
+    tw = {k: host(v) for k, v in model.tw_dev.items()}
+    H, d, T = sh.n_heads, sh.head_dim, sh.tokens_per_frame
+    nf = model.cache_len // T
+    ck = np.transpose(host(kp[:nf]), (0, 2, 1, 3)).reshape(-1, H, d)
+    cv = np.transpose(host(vp[:nf]), (0, 3, 1, 2)).reshape(-1, H, d)
+    x = host(model.xs[0])
+    ctxh = host(ctx)
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    m_t = O.time_modulation(TIMESTEPS[0], tw, sh.dim)
+    kc, vc = O.context_kv(ctxh, w, sh.eps)
+    t_ctx = time.perf_counter()
+    O.block_forward(x, ck, cv, model.cache_len // T, m_t, kc, vc, w, sh)
+    t1 = time.perf_counter()
+    return {"value": round((t1 - t_ctx) * 1e3, 1), "unit": "ms per chunk-denoise-step per block",
+            "cores": int(threads), "kind": "oracle",
+            "sample": ("one full block step (layer 0, t=1000) of the same workload: 4680 queries "
+                       "over 32760 keys, float64 numpy; text K/V and time modulation "
+                       f"({(t_ctx - t0) * 1e3:.0f} ms) excluded as on the GPU path")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the block's hot path is a one-GPU kernel "
+              "pipeline; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_15319_amd import ardit as A
+    from workloads import WORKLOADS
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = WORKLOADS["block13b"]
+    sh = wl.shape
+    cache_len = wl.cache_chunks[0] * sh.chunk_tokens
+    log(f"drawing {args.layers} layers on the device")
+    model = Model(A, sh, args.layers, cache_len, wl.ctx_len, dev)
+    torch.cuda.synchronize()
+    log("warmup")
+    for k in range(args.warmup):
+        model.step(k)
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    A.ardit_timing_collect()
+    A.ardit_timing_enable(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        model.step(k)
+    stop.record()
+    torch.cuda.synchronize()
+    A.ardit_timing_enable(False)
+    total_ms = start.elapsed_time(stop)
+    n_attn, attn_ms = A.ardit_timing_collect()
+    ms_step = total_ms / args.steps
+    ms_block = ms_step / args.layers
+    L_q, L_k, D = sh.chunk_tokens, cache_len + sh.chunk_tokens, sh.dim
+    attn_flops = 4.0 * L_q * L_k * D
+    attn_avg_ms = attn_ms / max(n_attn, 1)
+    achieved = attn_flops / (attn_avg_ms * 1e-3) / 1e12
+    log(f"{ms_step:.3f} ms/step, {ms_block:.4f} ms/block, attention {attn_avg_ms:.4f} ms "
+        f"({achieved:.1f} TFLOP/s) over {n_attn} launches")
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on one block step")
+        cpu = cpu_baseline(model)
+        log(f"oracle: {cpu['value']} ms on {cpu['cores']} threads")
+    line = {
+        "metric": "ms per chunk-denoise-step per block",
+        "value": round(ms_block, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normal draws, random-init weights)",
+        "config": {"workload": "1.3B-class AR-DiT block: D=1536, 12x128 heads, FFN 8960, "
+                               "chunk 4680 tokens (3x30x52) over a 28080-token cache, "
+                               "512 text tokens, 30 layers, t=1000/750/500/250",
+                   "layers": args.layers, "chunk_tokens": L_q, "kv_tokens": L_k,
+                   "ctx_tokens": wl.ctx_len},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "kernel": "paged self-attention",
+                     "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

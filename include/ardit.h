@@ -1,0 +1,215 @@
+/*
+ * ardit.h -- C ABI of the AR-DiT chunk-denoise block library (libardit.so).
+ *
+ * What is computed.  An autoregressive diffusion transformer generates video
+ * one chunk of latent frames at a time; every denoising step of a chunk runs
+ * the transformer stack on the chunk's tokens, each block attending over the
+ * stream's KV cache of earlier chunks plus the chunk itself, and the chunk is
+ * appended to that cache once generated (paper, Section 2.1, "AR-DiT").  The
+ * cache is paged at latent-frame granularity behind a logical page table, and
+ * different streams hold different cache lengths (Section 3.2, State Plane,
+ * and Section 4.4, unified KV management).  The block's internals are not
+ * given by the paper; this library computes, per block and per stream b:
+ *
+ *   M      = mod[b] + mod_table                       rows: shift1 scale1 gate1 shift2 scale2 gate2
+ *   h1     = rms(x) * (1 + scale1) + shift1
+ *   q,k,v  = split(h1 W_qkv^T + b_qkv)
+ *   q~,k~  = rope3d(rms(q) * g_q), rope3d(rms(k) * g_k)   (rms over the full width D)
+ *   K,V    = [cache | k~], [cache | v]                (k~, v written into the stream's pages)
+ *   o      = softmax(q~ K^T / sqrt(d)) V per head, every key visible
+ *   x1     = x + gate1 * (o W_o^T + b_o)
+ *   q_c    = rms(rms(x1) * g_n3 W_cq^T + b_cq) * g_cq
+ *   x2     = x1 + (softmax(q_c K_c^T / sqrt(d)) V_c) W_co^T + b_co
+ *   out    = x2 + gate2 * (GELU_tanh((rms(x2) * (1 + scale2) + shift2) W_1^T + b_1) W_2^T + b_2)
+ *
+ * with rms(z) = z / sqrt(mean(z^2) + eps), linears y = x W^T + b (W stored
+ * [out][in]), 3D RoPE over (latent frame, row, column) with head-dim
+ * segments (d - 4 floor(d/6), 2 floor(d/6), 2 floor(d/6)) and adjacent
+ * pairs, and K_c, V_c the per-stream text keys/values (ardit_ctx_kv).
+ *
+ * Conventions for every call below.
+ *  - Precision: activations, weights, pages and outputs are bf16; biases and
+ *    gains bf16; modulation tensors fp32.  All accumulation and all norm,
+ *    softmax, RoPE and GELU arithmetic is fp32; fp32 -> bf16 rounds to
+ *    nearest even.
+ *  - Ownership: the caller allocates and owns every buffer; the library
+ *    never allocates device memory in these calls and keeps no pointer after
+ *    the call returns.  "device" pointers are HIP device memory, "host"
+ *    pointers are read during the call only.
+ *  - Asynchrony: each call enqueues its kernels on `stream` and returns
+ *    without synchronising.  Host-side checks run before anything is
+ *    enqueued; when one fails the call returns a negative status, enqueues
+ *    nothing and leaves every output untouched.  A device-side failure shows
+ *    up as ARDIT_EHIP from a later call (ardit_last_error has the detail).
+ *  - Threading: calls may be made from several host threads; the last error
+ *    message is kept per thread.
+ *  - Layout of one frame page (T = lat_h * lat_w tokens of one latent frame,
+ *    H heads of d dims): keys [H][T][d], values transposed [H][d][T].  A
+ *    head's slice of a page is contiguous in both.  Logical token j of stream
+ *    b lives in page page_table[b * max_frames + j / T] at offset j % T.
+ *  - Text keys/values of stream b start at element offset ctx_off_b * D of
+ *    ctx_k / ctx_v, where ctx_off_b is the sum of the earlier streams'
+ *    ctx_lens; within a stream keys are [H][L_x][d] and values [H][d][L_x].
+ *  - Supported shapes: head_dim in {64, 128}; dim = n_heads * head_dim and
+ *    dim, ffn_dim multiples of 128; lat_h * lat_w a multiple of 8; at most
+ *    ARDIT_MAX_STREAMS streams per call.
+ */
+#ifndef ARDIT_H
+#define ARDIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARDIT_MAX_STREAMS 64
+#define ARDIT_TIME_FREQ_DIM 256
+
+typedef enum {
+  ARDIT_OK = 0,
+  ARDIT_EINVAL = -1,      /* null pointer or meaningless argument */
+  ARDIT_ESHAPE = -2,      /* dims inconsistent with each other or with a length */
+  ARDIT_ECAPACITY = -3,   /* a stream's keys exceed its page table or a length is out of range */
+  ARDIT_EWORKSPACE = -4,  /* workspace smaller than ardit_workspace_size reports */
+  ARDIT_EUNSUPPORTED = -5,/* shape outside what the kernels support (see above) */
+  ARDIT_EHIP = -6         /* the HIP runtime reported an error */
+} ardit_status;
+
+/* Model and chunk geometry (host struct). */
+typedef struct {
+  int32_t dim;               /* D, hidden width */
+  int32_t n_heads;           /* H */
+  int32_t head_dim;          /* d; D == H * d */
+  int32_t ffn_dim;           /* F */
+  int32_t frames_per_chunk;  /* latent frames per chunk (n_f) */
+  int32_t lat_h, lat_w;      /* latent grid of one frame; T = lat_h * lat_w tokens per frame page */
+  float eps;                 /* RMSNorm epsilon (1e-6) */
+  float rope_theta;          /* RoPE base (10000) */
+} ardit_dims;
+
+/* One batch of streams (host struct, host arrays of n_streams entries).
+ * Tokens of stream b occupy rows [sum_{b'<b} q_lens[b'], ... + q_lens[b]) of
+ * the packed activations. */
+typedef struct {
+  int32_t n_streams;          /* 1 .. ARDIT_MAX_STREAMS */
+  const int32_t* q_lens;      /* chunk tokens per stream; block calls: frames_per_chunk * T each */
+  const int32_t* cache_lens;  /* tokens already in the stream's cache; a multiple of T */
+  const int32_t* frame_pos0;  /* absolute latent-frame index of the chunk's first frame (RoPE t) */
+  const int32_t* ctx_lens;    /* text tokens per stream (>= 1) */
+} ardit_batch;
+
+/* Frame-paged KV cache of one layer (device memory). */
+typedef struct {
+  void* k_pages;               /* [n_pages][H][T][d] bf16 */
+  void* v_pages;               /* [n_pages][H][d][T] bf16 */
+  const int32_t* page_table;   /* [n_streams][max_frames] int32, physical page of each logical frame */
+  int32_t n_pages;             /* pages in the pool; out-of-range table entries are clamped into it */
+  int32_t max_frames;          /* row length of page_table */
+} ardit_kv_paged;
+
+/* Weights of one block (device pointers, bf16 unless noted, matrices [out][in]). */
+typedef struct {
+  const void *w_qkv, *b_qkv;   /* [3D][D], [3D]  rows: q, k, v */
+  const void *g_q, *g_k;       /* [D] QK-RMSNorm gains */
+  const void *w_o, *b_o;       /* [D][D], [D] */
+  const void *g_n3;            /* [D] cross-attention pre-norm gain */
+  const void *w_cq, *b_cq;     /* [D][D], [D] */
+  const void *g_cq;            /* [D] */
+  const void *w_ck, *b_ck;     /* [D][D], [D]   used by ardit_ctx_kv only */
+  const void *g_ck;            /* [D]           used by ardit_ctx_kv only */
+  const void *w_cv, *b_cv;     /* [D][D], [D]   used by ardit_ctx_kv only */
+  const void *w_co, *b_co;     /* [D][D], [D] */
+  const void *w_1, *b_1;       /* [F][D], [F] */
+  const void *w_2, *b_2;       /* [D][F], [D] */
+  const float* mod_table;      /* [6][D] fp32, added to the stream's time modulation */
+} ardit_block_weights;
+
+/* Shared time MLP (device pointers, bf16): 256 -> D -> D -> 6D. */
+typedef struct {
+  const void *w_t1, *b_t1;     /* [D][256], [D] */
+  const void *w_t2, *b_t2;     /* [D][D], [D] */
+  const void *w_m, *b_m;       /* [6D][D], [6D] */
+} ardit_time_weights;
+
+/* Name of a status code; never NULL. */
+const char* ardit_status_str(int status);
+/* Detail of the calling thread's last failed call ("" if none). */
+const char* ardit_last_error(void);
+/* ABI version (major * 100 + minor). */
+int ardit_version(void);
+
+/* Workspace bytes needed by any call below for this geometry and batch
+ * (block, stack, context and time-modulation calls share one workspace). */
+int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes);
+
+/* Time modulation, once per stream per denoising step: sinusoid of t (256
+ * features: cos then sin of t * 10000^(-k/128)), then
+ * m = W_m SiLU(W_t2 SiLU(W_t1 s + b_t1) + b_t2) + b_m.
+ * t_host: host [n_streams] timesteps.  mod_out: device fp32 [n_streams][6][D]. */
+int ardit_time_mod(hipStream_t stream, const ardit_dims* dims, int32_t n_streams,
+                   const float* t_host, const ardit_time_weights* tw, float* mod_out,
+                   void* ws, size_t ws_bytes);
+
+/* Text keys/values of each stream for one block: K_c = rms(ctx W_ck^T + b_ck) * g_ck,
+ * V_c = ctx W_cv^T + b_cv, written in the layout described above.
+ * ctx: device bf16 [sum ctx_lens][D], streams packed in order.  Only
+ * batch->n_streams and batch->ctx_lens are read. */
+int ardit_ctx_kv(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                 const void* ctx, const ardit_block_weights* w, void* ctx_k, void* ctx_v,
+                 void* ws, size_t ws_bytes);
+
+/* The QK-norm / RoPE / append step alone: from packed projections qkv
+ * (device bf16 [sum q_lens][3D], columns q | k | v), writes q~ (device bf16
+ * [sum q_lens][D]) and the chunk's k~ and v into logical slots
+ * [cache_len, cache_len + q_len) of each stream's pages.  g_q, g_k: device
+ * bf16 [D].  Nothing else of the pool is written. */
+int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                    const void* qkv, const void* g_q, const void* g_k,
+                    const ardit_kv_paged* kv, void* q_out);
+
+/* Paged attention alone: o = softmax(q K^T / sqrt(d)) V per stream and head
+ * over logical keys [0, cache_len + q_len) of the stream's pages (the chunk's
+ * own keys must already be in the pages).  q, o: device bf16 [sum q_lens][H][d]. */
+int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                   const void* q, const ardit_kv_paged* kv, void* o);
+
+/* One block, one stream.  x, out: device bf16 [L_q][D] (L_q = frames_per_chunk * T);
+ * kv.page_table has one row.  mod: device fp32 [6][D] (from ardit_time_mod).
+ * ctx_k / ctx_v from ardit_ctx_kv with ctx_len text tokens.  Writes the
+ * chunk's keys/values into slots [cache_len, cache_len + L_q); the caller
+ * commits the chunk by advancing cache_len (or rotating its page table). */
+int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x,
+                    ardit_kv_paged kv, int32_t cache_len, int32_t frame_pos0,
+                    const float* mod, const void* ctx_k, const void* ctx_v, int32_t ctx_len,
+                    const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes);
+
+/* One block over a ragged batch of streams sharing the weights (one GPU's share
+ * of the streams).  x, out: device bf16 [sum q_lens][D]; mod: device fp32
+ * [n_streams][6][D]; page_table rows follow the batch order. */
+int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                           const void* x, const ardit_kv_paged* kv, const float* mod,
+                           const void* ctx_k, const void* ctx_v, const ardit_block_weights* w,
+                           void* out, void* ws, size_t ws_bytes);
+
+/* n_layers blocks applied in sequence (one denoising step of the stack).
+ * kv, w, ctx_k, ctx_v: host arrays of n_layers entries.  x is not modified. */
+int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                    int32_t n_layers, const void* x, const ardit_kv_paged* kv, const float* mod,
+                    const void* const* ctx_k, const void* const* ctx_v,
+                    const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes);
+
+/* Kernel timing: while enabled, block calls record HIP events on their stream
+ * around every launch of the self-attention kernel.  ardit_timing_collect
+ * waits for the recorded events, returns the number of launches and their
+ * summed duration in ms, and clears the record. */
+int ardit_timing_enable(int enable);
+int ardit_timing_collect(int32_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARDIT_H */

@@ -1,0 +1,266 @@
+"""ctypes binding of libardit (include/ardit.h).
+
+Argument marshalling only: every function forwards to the C entry point of
+the same name.  Tensor arguments may be torch tensors (their data_ptr() is
+passed) or raw integer device addresses; `stream` is a HIP stream handle
+(int) or None for torch's current stream.  The library must have been built
+(``python -m paper_2606_15319_amd.build``); importing this module without it
+raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libardit.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_15319_amd.build`")
+# The library must run on the same HIP runtime instance as the framework that
+# owns the streams and memory handed to it.  torch bundles its own
+# libamdhip64.so.7; loading torch first makes the library's dependency on that
+# soname resolve to torch's copy instead of pulling in a second runtime.
+try:
+    import torch  # noqa: F401
+except ImportError:  # plain C-ABI use without torch
+    pass
+_lib = C.CDLL(LIB_PATH)
+
+ARDIT_MAX_STREAMS = 64
+STATUS = {0: "ARDIT_OK", -1: "ARDIT_EINVAL", -2: "ARDIT_ESHAPE", -3: "ARDIT_ECAPACITY",
+          -4: "ARDIT_EWORKSPACE", -5: "ARDIT_EUNSUPPORTED", -6: "ARDIT_EHIP"}
+
+
+class ArditError(RuntimeError):
+    def __init__(self, status: int, func: str, detail: str):
+        super().__init__(f"{func}: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.func = func
+        self.detail = detail
+
+
+# ------------------------------------------------------------------ structs
+class ardit_dims(C.Structure):
+    _fields_ = [("dim", C.c_int32), ("n_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("ffn_dim", C.c_int32), ("frames_per_chunk", C.c_int32),
+                ("lat_h", C.c_int32), ("lat_w", C.c_int32),
+                ("eps", C.c_float), ("rope_theta", C.c_float)]
+
+
+class ardit_batch(C.Structure):
+    _fields_ = [("n_streams", C.c_int32), ("q_lens", C.POINTER(C.c_int32)),
+                ("cache_lens", C.POINTER(C.c_int32)), ("frame_pos0", C.POINTER(C.c_int32)),
+                ("ctx_lens", C.POINTER(C.c_int32))]
+
+
+class ardit_kv_paged(C.Structure):
+    _fields_ = [("k_pages", C.c_void_p), ("v_pages", C.c_void_p), ("page_table", C.c_void_p),
+                ("n_pages", C.c_int32), ("max_frames", C.c_int32)]
+
+
+_BLOCK_FIELDS = ("w_qkv", "b_qkv", "g_q", "g_k", "w_o", "b_o", "g_n3", "w_cq", "b_cq", "g_cq",
+                 "w_ck", "b_ck", "g_ck", "w_cv", "b_cv", "w_co", "b_co", "w_1", "b_1", "w_2",
+                 "b_2", "mod_table")
+_TIME_FIELDS = ("w_t1", "b_t1", "w_t2", "b_t2", "w_m", "b_m")
+
+
+class ardit_block_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _BLOCK_FIELDS]
+
+
+class ardit_time_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in _TIME_FIELDS]
+
+
+_vp, _i32, _sz = C.c_void_p, C.c_int32, C.c_size_t
+_P = C.POINTER
+_SIGS = {
+    "ardit_status_str": (C.c_char_p, [C.c_int]),
+    "ardit_last_error": (C.c_char_p, []),
+    "ardit_version": (C.c_int, []),
+    "ardit_workspace_size": (C.c_int, [_P(ardit_dims), _P(ardit_batch), _P(_sz)]),
+    "ardit_time_mod": (C.c_int, [_vp, _P(ardit_dims), _i32, _P(C.c_float),
+                                 _P(ardit_time_weights), _vp, _vp, _sz]),
+    "ardit_ctx_kv": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
+                               _P(ardit_block_weights), _vp, _vp, _vp, _sz]),
+    "ardit_kv_append": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp, _vp, _vp,
+                                  _P(ardit_kv_paged), _vp]),
+    "ardit_attn_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
+                                 _P(ardit_kv_paged), _vp]),
+    "ardit_block_fwd": (C.c_int, [_vp, _P(ardit_dims), _vp, ardit_kv_paged, _i32, _i32, _vp,
+                                  _vp, _vp, _i32, _P(ardit_block_weights), _vp, _vp, _sz]),
+    "ardit_block_fwd_varlen": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
+                                         _P(ardit_kv_paged), _vp, _vp, _vp,
+                                         _P(ardit_block_weights), _vp, _vp, _sz]),
+    "ardit_stack_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _i32, _vp,
+                                  _P(ardit_kv_paged), _vp, _P(_vp), _P(_vp),
+                                  _P(ardit_block_weights), _vp, _vp, _sz]),
+    "ardit_timing_enable": (C.c_int, [C.c_int]),
+    "ardit_timing_collect": (C.c_int, [_P(_i32), _P(C.c_double)]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+def exported_symbols():
+    return tuple(_SIGS)
+
+
+def has_symbol(name: str) -> bool:
+    try:
+        getattr(_lib, name)
+        return True
+    except AttributeError:
+        return False
+
+
+# ---------------------------------------------------------------- helpers
+def _ptr(x) -> int:
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return int(s) if not hasattr(s, "cuda_stream") else s.cuda_stream
+
+
+def _check(status: int, func: str):
+    if status != 0:
+        raise ArditError(status, func, ardit_last_error())
+
+
+def ardit_status_str(status: int) -> str:
+    return _lib.ardit_status_str(status).decode()
+
+
+def ardit_last_error() -> str:
+    return _lib.ardit_last_error().decode()
+
+
+def ardit_version() -> int:
+    return _lib.ardit_version()
+
+
+def make_dims(dim, n_heads, head_dim, ffn_dim, frames_per_chunk, lat_h, lat_w, eps=1e-6,
+              rope_theta=10000.0) -> ardit_dims:
+    return ardit_dims(dim, n_heads, head_dim, ffn_dim, frames_per_chunk, lat_h, lat_w, eps,
+                      rope_theta)
+
+
+def dims_from_shape(shape) -> ardit_dims:
+    """From any object with dim, n_heads, head_dim, ffn_dim, frames, lat_h, lat_w, eps, theta."""
+    return make_dims(shape.dim, shape.n_heads, shape.head_dim, shape.ffn_dim, shape.frames,
+                     shape.lat_h, shape.lat_w, shape.eps, shape.theta)
+
+
+class Batch:
+    """Host-side batch descriptor; keeps its int32 arrays alive."""
+
+    def __init__(self, q_lens=None, cache_lens=None, frame_pos0=None, ctx_lens=None):
+        lens = [a for a in (q_lens, cache_lens, frame_pos0, ctx_lens) if a is not None]
+        n = len(lens[0]) if lens else 0
+        self._arrs = []
+
+        def arr(a):
+            if a is None:
+                return None
+            assert len(a) == n, "all per-stream arrays must have the same length"
+            c = (C.c_int32 * n)(*[int(v) for v in a])
+            self._arrs.append(c)
+            return C.cast(c, C.POINTER(C.c_int32))
+
+        self.struct = ardit_batch(n, arr(q_lens), arr(cache_lens), arr(frame_pos0), arr(ctx_lens))
+        self.n = n
+
+
+def kv_paged(k_pages, v_pages, page_table, n_pages: int, max_frames: int) -> ardit_kv_paged:
+    return ardit_kv_paged(_ptr(k_pages), _ptr(v_pages), _ptr(page_table), int(n_pages),
+                          int(max_frames))
+
+
+def block_weights(w: dict) -> ardit_block_weights:
+    return ardit_block_weights(*[_ptr(w.get(n)) for n in _BLOCK_FIELDS])
+
+
+def time_weights(w: dict) -> ardit_time_weights:
+    return ardit_time_weights(*[_ptr(w[n]) for n in _TIME_FIELDS])
+
+
+# ------------------------------------------------------------ entry points
+def ardit_workspace_size(dims: ardit_dims, batch: Batch) -> int:
+    n = C.c_size_t(0)
+    _check(_lib.ardit_workspace_size(C.byref(dims), C.byref(batch.struct), C.byref(n)),
+           "ardit_workspace_size")
+    return n.value
+
+
+def ardit_time_mod(stream, dims, t_values, tw: ardit_time_weights, mod_out, ws, ws_bytes):
+    t = (C.c_float * len(t_values))(*[float(v) for v in t_values])
+    _check(_lib.ardit_time_mod(_stream(stream), C.byref(dims), len(t_values), t, C.byref(tw),
+                               _ptr(mod_out), _ptr(ws), int(ws_bytes)), "ardit_time_mod")
+
+
+def ardit_ctx_kv(stream, dims, batch: Batch, ctx, w: ardit_block_weights, ctx_k, ctx_v, ws,
+                 ws_bytes):
+    _check(_lib.ardit_ctx_kv(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(ctx),
+                             C.byref(w), _ptr(ctx_k), _ptr(ctx_v), _ptr(ws), int(ws_bytes)),
+           "ardit_ctx_kv")
+
+
+def ardit_kv_append(stream, dims, batch: Batch, qkv, g_q, g_k, kv: ardit_kv_paged, q_out):
+    _check(_lib.ardit_kv_append(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(qkv),
+                                _ptr(g_q), _ptr(g_k), C.byref(kv), _ptr(q_out)),
+           "ardit_kv_append")
+
+
+def ardit_attn_fwd(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o):
+    _check(_lib.ardit_attn_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(q),
+                               C.byref(kv), _ptr(o)), "ardit_attn_fwd")
+
+
+def ardit_block_fwd(stream, dims, x, kv: ardit_kv_paged, cache_len, frame_pos0, mod, ctx_k,
+                    ctx_v, ctx_len, w: ardit_block_weights, out, ws, ws_bytes):
+    _check(_lib.ardit_block_fwd(_stream(stream), C.byref(dims), _ptr(x), kv, int(cache_len),
+                                int(frame_pos0), _ptr(mod), _ptr(ctx_k), _ptr(ctx_v),
+                                int(ctx_len), C.byref(w), _ptr(out), _ptr(ws), int(ws_bytes)),
+           "ardit_block_fwd")
+
+
+def ardit_block_fwd_varlen(stream, dims, batch: Batch, x, kv: ardit_kv_paged, mod, ctx_k, ctx_v,
+                           w: ardit_block_weights, out, ws, ws_bytes):
+    _check(_lib.ardit_block_fwd_varlen(_stream(stream), C.byref(dims), C.byref(batch.struct),
+                                       _ptr(x), C.byref(kv), _ptr(mod), _ptr(ctx_k), _ptr(ctx_v),
+                                       C.byref(w), _ptr(out), _ptr(ws), int(ws_bytes)),
+           "ardit_block_fwd_varlen")
+
+
+def ardit_stack_fwd(stream, dims, batch: Batch, x, kvs, mod, ctx_ks, ctx_vs, ws_list, out, ws,
+                    ws_bytes):
+    L = len(kvs)
+    kv_arr = (ardit_kv_paged * L)(*kvs)
+    w_arr = (ardit_block_weights * L)(*ws_list)
+    ck = (C.c_void_p * L)(*[_ptr(t) for t in ctx_ks])
+    cv = (C.c_void_p * L)(*[_ptr(t) for t in ctx_vs])
+    _check(_lib.ardit_stack_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), L, _ptr(x),
+                                kv_arr, _ptr(mod), ck, cv, w_arr, _ptr(out), _ptr(ws),
+                                int(ws_bytes)), "ardit_stack_fwd")
+
+
+def ardit_timing_enable(enable: bool):
+    _check(_lib.ardit_timing_enable(1 if enable else 0), "ardit_timing_enable")
+
+
+def ardit_timing_collect():
+    n = C.c_int32(0)
+    ms = C.c_double(0.0)
+    _check(_lib.ardit_timing_collect(C.byref(n), C.byref(ms)), "ardit_timing_collect")
+    return n.value, ms.value

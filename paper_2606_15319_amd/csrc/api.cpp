@@ -1,0 +1,673 @@
+// C ABI of libardit: argument validation, workspace layout and the launch
+// chains of the block.  Every check runs before the first launch, so a
+// failing call enqueues nothing and leaves its outputs untouched.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "ardit.h"
+#include "launch.h"
+
+using namespace ardit;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(ARDIT_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define ARDIT_TRY(expr)                        \
+  do {                                         \
+    int _s = (expr);                           \
+    if (_s != ARDIT_OK) return _s;             \
+  } while (0)
+
+#define ARDIT_HIP(expr, what)                  \
+  do {                                         \
+    hipError_t _e = (expr);                    \
+    if (_e != hipSuccess) return hip_fail(_e, what); \
+  } while (0)
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+int check_dims(const ardit_dims* d) {
+  if (!d) return fail(ARDIT_EINVAL, "dims is NULL");
+  if (d->dim <= 0 || d->n_heads <= 0 || d->head_dim <= 0 || d->ffn_dim <= 0 ||
+      d->frames_per_chunk <= 0 || d->lat_h <= 0 || d->lat_w <= 0)
+    return fail(ARDIT_ESHAPE, "dims must be positive");
+  if (static_cast<int64_t>(d->n_heads) * d->head_dim != d->dim)
+    return fail(ARDIT_ESHAPE, "dim %d != n_heads %d * head_dim %d", d->dim, d->n_heads,
+                d->head_dim);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(ARDIT_EUNSUPPORTED, "head_dim %d not in {64, 128}", d->head_dim);
+  if (d->dim % 128 != 0 || d->ffn_dim % 128 != 0)
+    return fail(ARDIT_EUNSUPPORTED, "dim %d and ffn_dim %d must be multiples of 128", d->dim,
+                d->ffn_dim);
+  if (d->dim > 8192) return fail(ARDIT_EUNSUPPORTED, "dim %d above 8192", d->dim);
+  if (d->ffn_dim > 65536) return fail(ARDIT_EUNSUPPORTED, "ffn_dim %d above 65536", d->ffn_dim);
+  const int64_t T = static_cast<int64_t>(d->lat_h) * d->lat_w;
+  if (T % 8 != 0) return fail(ARDIT_EUNSUPPORTED, "lat_h * lat_w = %lld not a multiple of 8",
+                              static_cast<long long>(T));
+  if (T * d->frames_per_chunk > (1 << 20)) return fail(ARDIT_ESHAPE, "chunk too large");
+  if (!(d->eps > 0.f) || !(d->rope_theta > 0.f))
+    return fail(ARDIT_EINVAL, "eps and rope_theta must be positive");
+  return ARDIT_OK;
+}
+
+int tokens_per_frame(const ardit_dims* d) { return d->lat_h * d->lat_w; }
+int chunk_tokens(const ardit_dims* d) { return d->frames_per_chunk * tokens_per_frame(d); }
+
+enum BatchUse : unsigned {
+  kUseQ = 1, kUseCache = 2, kUsePos = 4, kUseCtx = 8, kChunkQ = 16,
+};
+
+int check_batch(const ardit_dims* d, const ardit_batch* b, unsigned use) {
+  if (!b) return fail(ARDIT_EINVAL, "batch is NULL");
+  if (b->n_streams < 1 || b->n_streams > ARDIT_MAX_STREAMS)
+    return fail(ARDIT_EINVAL, "n_streams %d not in [1, %d]", b->n_streams, ARDIT_MAX_STREAMS);
+  if ((use & kUseQ) && !b->q_lens) return fail(ARDIT_EINVAL, "batch q_lens is NULL");
+  if ((use & kUseCache) && !b->cache_lens) return fail(ARDIT_EINVAL, "batch cache_lens is NULL");
+  if ((use & kUsePos) && !b->frame_pos0) return fail(ARDIT_EINVAL, "batch frame_pos0 is NULL");
+  if ((use & kUseCtx) && !b->ctx_lens) return fail(ARDIT_EINVAL, "batch ctx_lens is NULL");
+  const int T = tokens_per_frame(d);
+  int64_t nq = 0, nc = 0;
+  for (int i = 0; i < b->n_streams; ++i) {
+    if (use & kUseQ) {
+      const int q = b->q_lens[i];
+      if (q < 0) return fail(ARDIT_ESHAPE, "q_lens[%d] = %d is negative", i, q);
+      if ((use & kChunkQ) && q != chunk_tokens(d))
+        return fail(ARDIT_ESHAPE, "q_lens[%d] = %d != frames_per_chunk * lat_h * lat_w = %d", i, q,
+                    chunk_tokens(d));
+      nq += q;
+    }
+    if (use & kUseCache) {
+      const int c = b->cache_lens[i];
+      if (c < 0 || c % T != 0)
+        return fail(ARDIT_ESHAPE, "cache_lens[%d] = %d is not a non-negative multiple of %d", i,
+                    c, T);
+    }
+    if ((use & kUsePos) && b->frame_pos0[i] < 0)
+      return fail(ARDIT_EINVAL, "frame_pos0[%d] = %d is negative", i, b->frame_pos0[i]);
+    if (use & kUseCtx) {
+      const int c = b->ctx_lens[i];
+      if (c < 1) return fail(ARDIT_ESHAPE, "ctx_lens[%d] = %d must be >= 1", i, c);
+      nc += c;
+    }
+  }
+  if (nq > (1 << 22) || nc > (1 << 22))
+    return fail(ARDIT_ECAPACITY, "more than 2^22 tokens in one batch");
+  return ARDIT_OK;
+}
+
+int check_kv(const ardit_dims* d, const ardit_batch* b, const ardit_kv_paged* kv) {
+  if (!kv) return fail(ARDIT_EINVAL, "kv is NULL");
+  if (!kv->k_pages || !kv->v_pages || !kv->page_table)
+    return fail(ARDIT_EINVAL, "kv pointers must be non-NULL");
+  if (misaligned(kv->k_pages) || misaligned(kv->v_pages))
+    return fail(ARDIT_EINVAL, "kv pages must be 16-byte aligned");
+  if (kv->n_pages < 1 || kv->max_frames < 1)
+    return fail(ARDIT_EINVAL, "n_pages and max_frames must be >= 1");
+  const int64_t T = tokens_per_frame(d);
+  if (static_cast<int64_t>(kv->n_pages) * d->dim * T > (int64_t(1) << 40))
+    return fail(ARDIT_ECAPACITY, "page pool too large");
+  for (int i = 0; i < b->n_streams; ++i) {
+    const int64_t keys = static_cast<int64_t>(b->cache_lens[i]) + b->q_lens[i];
+    const int64_t frames = (keys + T - 1) / T;
+    if (frames > kv->max_frames)
+      return fail(ARDIT_ECAPACITY, "stream %d needs %lld frames > max_frames %d", i,
+                  static_cast<long long>(frames), kv->max_frames);
+  }
+  return ARDIT_OK;
+}
+
+int check_ptr(const void* p, const char* name) {
+  if (!p) return fail(ARDIT_EINVAL, "%s is NULL", name);
+  if (misaligned(p)) return fail(ARDIT_EINVAL, "%s must be 16-byte aligned", name);
+  return ARDIT_OK;
+}
+
+int check_block_weights(const ardit_block_weights* w, bool ctx) {
+  if (!w) return fail(ARDIT_EINVAL, "weights is NULL");
+  if (ctx) {
+    ARDIT_TRY(check_ptr(w->w_ck, "w_ck"));
+    ARDIT_TRY(check_ptr(w->b_ck, "b_ck"));
+    ARDIT_TRY(check_ptr(w->g_ck, "g_ck"));
+    ARDIT_TRY(check_ptr(w->w_cv, "w_cv"));
+    ARDIT_TRY(check_ptr(w->b_cv, "b_cv"));
+    return ARDIT_OK;
+  }
+  const void* p[] = {w->w_qkv, w->b_qkv, w->g_q, w->g_k, w->w_o, w->b_o, w->g_n3, w->w_cq,
+                     w->b_cq, w->g_cq, w->w_co, w->b_co, w->w_1, w->b_1, w->w_2, w->b_2,
+                     w->mod_table};
+  const char* n[] = {"w_qkv", "b_qkv", "g_q", "g_k", "w_o", "b_o", "g_n3", "w_cq", "b_cq",
+                     "g_cq", "w_co", "b_co", "w_1", "b_1", "w_2", "b_2", "mod_table"};
+  for (size_t i = 0; i < sizeof(p) / sizeof(p[0]); ++i) ARDIT_TRY(check_ptr(p[i], n[i]));
+  return ARDIT_OK;
+}
+
+// ------------------------------------------------------------ workspace
+constexpr size_t kAlign = 256;
+size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Ws {
+  size_t tsin, te1, te2;             // fp32 time-MLP scratch
+  size_t h, qkv, q, o, x1, x2, u;    // bf16 block activations
+  size_t ck, cv;                     // bf16 text projections
+  size_t total;
+};
+
+Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc) {
+  Ws w;
+  size_t off = 0;
+  const size_t D = d->dim, F = d->ffn_dim;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += up(bytes);
+    return o;
+  };
+  w.tsin = take(sizeof(float) * B * ARDIT_TIME_FREQ_DIM);
+  w.te1 = take(sizeof(float) * B * D);
+  w.te2 = take(sizeof(float) * B * D);
+  w.h = take(2 * N * D);
+  w.qkv = take(2 * N * 3 * D);
+  w.q = take(2 * N * D);
+  w.o = take(2 * N * D);
+  w.x1 = take(2 * N * D);
+  w.x2 = take(2 * N * D);
+  w.u = take(2 * N * F);
+  w.ck = take(2 * Nc * D);
+  w.cv = take(2 * Nc * D);
+  w.total = off;
+  return w;
+}
+
+int64_t sum_q(const ardit_batch* b) {
+  int64_t n = 0;
+  if (b->q_lens)
+    for (int i = 0; i < b->n_streams; ++i) n += b->q_lens[i];
+  return n;
+}
+int64_t sum_ctx(const ardit_batch* b) {
+  int64_t n = 0;
+  if (b->ctx_lens)
+    for (int i = 0; i < b->n_streams; ++i) n += b->ctx_lens[i];
+  return n;
+}
+
+int check_ws(const ardit_dims* d, const ardit_batch* b, const void* ws, size_t ws_bytes,
+             Ws* out) {
+  *out = ws_layout(d, b->n_streams, sum_q(b), sum_ctx(b));
+  if (!ws) return fail(ARDIT_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+    return fail(ARDIT_EINVAL, "workspace must be %zu-byte aligned", kAlign);
+  if (ws_bytes < out->total)
+    return fail(ARDIT_EWORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, out->total);
+  return ARDIT_OK;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+RowStreams q_streams(const ardit_batch* b) {
+  RowStreams rs;
+  rs.n = b->n_streams;
+  int row = 0;
+  for (int i = 0; i < b->n_streams; ++i) {
+    rs.s[i].row_begin = row;
+    rs.s[i].len = b->q_lens[i];
+    rs.s[i].cache_len = b->cache_lens ? b->cache_lens[i] : 0;
+    rs.s[i].frame_pos0 = b->frame_pos0 ? b->frame_pos0[i] : 0;
+    row += b->q_lens[i];
+  }
+  return rs;
+}
+
+RowStreams ctx_streams(const ardit_batch* b) {
+  RowStreams rs;
+  rs.n = b->n_streams;
+  int row = 0;
+  for (int i = 0; i < b->n_streams; ++i) {
+    rs.s[i].row_begin = row;
+    rs.s[i].len = b->ctx_lens[i];
+    rs.s[i].cache_len = 0;
+    rs.s[i].frame_pos0 = 0;
+    row += b->ctx_lens[i];
+  }
+  return rs;
+}
+
+// ---------------------------------------------------------------- timing
+struct Timing {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> rec;
+};
+Timing& timing() {
+  static Timing t;
+  return t;
+}
+
+hipEvent_t take_event(Timing& t) {
+  if (!t.pool.empty()) {
+    hipEvent_t e = t.pool.back();
+    t.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// launches the self-attention kernel, bracketed by events while timing is on
+int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
+  Timing& tm = timing();
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  {
+    std::lock_guard<std::mutex> g(tm.mu);
+    if (tm.enabled) {
+      e0 = take_event(tm);
+      e1 = take_event(tm);
+    }
+  }
+  if (e0 && e1) ARDIT_HIP(hipEventRecord(e0, st), "hipEventRecord");
+  ARDIT_HIP(launch_attention(st, a, hd, true), "self-attention launch");
+  if (e0 && e1) {
+    ARDIT_HIP(hipEventRecord(e1, st), "hipEventRecord");
+    std::lock_guard<std::mutex> g(tm.mu);
+    tm.rec.emplace_back(e0, e1);
+  }
+  return ARDIT_OK;
+}
+
+AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
+                        const ardit_kv_paged* kv, void* o) {
+  AttnArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = static_cast<const bf16_t*>(q);
+  a.ldq = d->dim;
+  a.o = static_cast<bf16_t*>(o);
+  a.ldo = d->dim;
+  a.k = static_cast<const bf16_t*>(kv->k_pages);
+  a.v = static_cast<const bf16_t*>(kv->v_pages);
+  a.page_table = kv->page_table;
+  a.max_frames = kv->max_frames;
+  a.n_pages = kv->n_pages;
+  a.T = tokens_per_frame(d);
+  a.fT = make_fastdiv(a.T);
+  a.H = d->n_heads;
+  a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d->head_dim)));
+  a.n_streams = b->n_streams;
+  int row = 0;
+  for (int i = 0; i < b->n_streams; ++i) {
+    AttnStream& s = a.s[i];
+    s.q_off = row;
+    s.q_len = b->q_lens[i];
+    s.kv_len = b->cache_lens[i] + b->q_lens[i];
+    s.stream = i;
+    s.base_off = 0;
+    s.T = a.T;
+    row += b->q_lens[i];
+  }
+  plan_attention(a, d->head_dim);
+  return a;
+}
+
+AttnArgs cross_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
+                         const void* ctx_k, const void* ctx_v, void* o) {
+  AttnArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = static_cast<const bf16_t*>(q);
+  a.ldq = d->dim;
+  a.o = static_cast<bf16_t*>(o);
+  a.ldo = d->dim;
+  a.k = static_cast<const bf16_t*>(ctx_k);
+  a.v = static_cast<const bf16_t*>(ctx_v);
+  a.T = 1;
+  a.fT = make_fastdiv(1);
+  a.H = d->n_heads;
+  a.scale_log2 = static_cast<float>(1.4426950408889634 / sqrt(static_cast<double>(d->head_dim)));
+  a.n_streams = b->n_streams;
+  int row = 0, crow = 0;
+  for (int i = 0; i < b->n_streams; ++i) {
+    AttnStream& s = a.s[i];
+    s.q_off = row;
+    s.q_len = b->q_lens[i];
+    s.kv_len = b->ctx_lens[i];
+    s.stream = i;
+    s.base_off = crow * d->dim;
+    s.T = b->ctx_lens[i];
+    row += b->q_lens[i];
+    crow += b->ctx_lens[i];
+  }
+  plan_attention(a, d->head_dim);
+  return a;
+}
+
+// the block chain on validated arguments
+int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const void* xin,
+                const ardit_kv_paged* kv, const float* mod, const void* ctx_k, const void* ctx_v,
+                const ardit_block_weights* w, void* out, void* ws, const Ws& L) {
+  const int N = static_cast<int>(sum_q(b));
+  const int D = d->dim, F = d->ffn_dim, H = d->n_heads, hd = d->head_dim;
+  const int Lq = chunk_tokens(d);
+  const bf16_t* x = static_cast<const bf16_t*>(xin);
+  bf16_t* h = at<bf16_t>(ws, L.h);
+  bf16_t* qkv = at<bf16_t>(ws, L.qkv);
+  bf16_t* q = at<bf16_t>(ws, L.q);
+  bf16_t* o = at<bf16_t>(ws, L.o);
+  bf16_t* x1 = at<bf16_t>(ws, L.x1);
+  bf16_t* x2 = at<bf16_t>(ws, L.x2);
+  bf16_t* u = at<bf16_t>(ws, L.u);
+  bf16_t* y = static_cast<bf16_t*>(out);
+  const float* mt = w->mod_table;
+  const RowStreams rs = q_streams(b);
+  auto B16 = [](const void* p) { return static_cast<const bf16_t*>(p); };
+
+  // adaLN RMSNorm #1 and the QKV projection
+  ARDIT_HIP(launch_adaln_norm(st, x, h, N, D, mod, mt, 0, 1, Lq, d->eps), "adaln_norm");
+  GemmEpiArgs e;
+  e.bias = B16(w->b_qkv);
+  ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_qkv), D, qkv, 3 * D, N, 3 * D, D, e),
+            "qkv gemm");
+  // QK-norm, 3D RoPE, append k~ and v to the pages
+  RopeGeom rg{D, H, hd, tokens_per_frame(d), d->lat_w, kv->max_frames, kv->n_pages, d->eps,
+              d->rope_theta};
+  ARDIT_HIP(launch_qk_norm_rope(st, qkv, N, rg, B16(w->g_q), B16(w->g_k), q,
+                                static_cast<bf16_t*>(kv->k_pages), kv->page_table, rs),
+            "qk_norm_rope");
+  ARDIT_HIP(launch_v_transpose(st, qkv, 3 * D, 2 * D, N, D, H, hd,
+                               static_cast<bf16_t*>(kv->v_pages), true, tokens_per_frame(d),
+                               kv->page_table, kv->max_frames, kv->n_pages, rs),
+            "v_append");
+  // self-attention over [cache | chunk]
+  const AttnArgs sa = self_attn_args(d, b, q, kv, o);
+  ARDIT_TRY(run_self_attention(st, sa, hd));
+  // x1 = x + gate1 * (o W_o^T + b_o)
+  e = GemmEpiArgs();
+  e.bias = B16(w->b_o);
+  e.res = x;
+  e.ldr = D;
+  e.mod = mod;
+  e.mod_table = mt;
+  e.gate_row = 2;
+  e.dim = D;
+  e.rows_per_stream = Lq;
+  ARDIT_HIP(launch_gemm(st, kEpiBiasGateRes, o, D, B16(w->w_o), D, x1, D, N, D, D, e), "o gemm");
+  // cross-attention query: rms(rms(x1) g_n3 W_cq^T + b_cq) g_cq
+  ARDIT_HIP(launch_rms_gain(st, x1, h, N, D, B16(w->g_n3), d->eps), "cross pre-norm");
+  e = GemmEpiArgs();
+  e.bias = B16(w->b_cq);
+  ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_cq), D, q, D, N, D, D, e), "cq gemm");
+  ARDIT_HIP(launch_rms_gain(st, q, q, N, D, B16(w->g_cq), d->eps), "cross q-norm");
+  const AttnArgs ca = cross_attn_args(d, b, q, ctx_k, ctx_v, o);
+  ARDIT_HIP(launch_attention(st, ca, hd, false), "cross-attention");
+  // x2 = x1 + o_c W_co^T + b_co
+  e = GemmEpiArgs();
+  e.bias = B16(w->b_co);
+  e.res = x1;
+  e.ldr = D;
+  ARDIT_HIP(launch_gemm(st, kEpiBiasRes, o, D, B16(w->w_co), D, x2, D, N, D, D, e), "co gemm");
+  // FFN: out = x2 + gate2 * (GELU(adaLN2(x2) W_1^T + b_1) W_2^T + b_2)
+  ARDIT_HIP(launch_adaln_norm(st, x2, h, N, D, mod, mt, 3, 4, Lq, d->eps), "adaln_norm 2");
+  e = GemmEpiArgs();
+  e.bias = B16(w->b_1);
+  ARDIT_HIP(launch_gemm(st, kEpiBiasGelu, h, D, B16(w->w_1), D, u, F, N, F, D, e), "ffn up");
+  e = GemmEpiArgs();
+  e.bias = B16(w->b_2);
+  e.res = x2;
+  e.ldr = D;
+  e.mod = mod;
+  e.mod_table = mt;
+  e.gate_row = 5;
+  e.dim = D;
+  e.rows_per_stream = Lq;
+  ARDIT_HIP(launch_gemm(st, kEpiBiasGateRes, u, F, B16(w->w_2), F, y, D, N, D, F, e), "ffn down");
+  return ARDIT_OK;
+}
+
+int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
+                     const ardit_kv_paged* kv, const float* mod, const void* ctx_k,
+                     const void* ctx_v, const ardit_block_weights* w, const void* out) {
+  ARDIT_TRY(check_dims(d));
+  ARDIT_TRY(check_batch(d, b, kUseQ | kUseCache | kUsePos | kUseCtx | kChunkQ));
+  ARDIT_TRY(check_kv(d, b, kv));
+  ARDIT_TRY(check_ptr(x, "x"));
+  ARDIT_TRY(check_ptr(out, "out"));
+  ARDIT_TRY(check_ptr(mod, "mod"));
+  ARDIT_TRY(check_ptr(ctx_k, "ctx_k"));
+  ARDIT_TRY(check_ptr(ctx_v, "ctx_v"));
+  ARDIT_TRY(check_block_weights(w, false));
+  return ARDIT_OK;
+}
+
+}  // namespace
+
+// ======================================================================== ABI
+extern "C" {
+
+const char* ardit_status_str(int s) {
+  switch (s) {
+    case ARDIT_OK: return "ARDIT_OK";
+    case ARDIT_EINVAL: return "ARDIT_EINVAL";
+    case ARDIT_ESHAPE: return "ARDIT_ESHAPE";
+    case ARDIT_ECAPACITY: return "ARDIT_ECAPACITY";
+    case ARDIT_EWORKSPACE: return "ARDIT_EWORKSPACE";
+    case ARDIT_EUNSUPPORTED: return "ARDIT_EUNSUPPORTED";
+    case ARDIT_EHIP: return "ARDIT_EHIP";
+    default: return "ARDIT_UNKNOWN";
+  }
+}
+
+const char* ardit_last_error(void) { return g_last_error.c_str(); }
+
+int ardit_version(void) { return 100; }
+
+int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) {
+  ARDIT_TRY(check_dims(dims));
+  if (!bytes) return fail(ARDIT_EINVAL, "bytes is NULL");
+  ARDIT_TRY(check_batch(dims, batch, 0));
+  if (batch->q_lens) ARDIT_TRY(check_batch(dims, batch, kUseQ));
+  if (batch->ctx_lens) ARDIT_TRY(check_batch(dims, batch, kUseCtx));
+  *bytes = ws_layout(dims, batch->n_streams, sum_q(batch), sum_ctx(batch)).total;
+  return ARDIT_OK;
+}
+
+int ardit_time_mod(hipStream_t stream, const ardit_dims* dims, int32_t n_streams,
+                   const float* t_host, const ardit_time_weights* tw, float* mod_out, void* ws,
+                   size_t ws_bytes) {
+  ARDIT_TRY(check_dims(dims));
+  if (n_streams < 1 || n_streams > ARDIT_MAX_STREAMS)
+    return fail(ARDIT_EINVAL, "n_streams %d not in [1, %d]", n_streams, ARDIT_MAX_STREAMS);
+  if (!t_host) return fail(ARDIT_EINVAL, "t_host is NULL");
+  if (!tw) return fail(ARDIT_EINVAL, "time weights NULL");
+  const void* p[] = {tw->w_t1, tw->b_t1, tw->w_t2, tw->b_t2, tw->w_m, tw->b_m, mod_out, ws};
+  const char* n[] = {"w_t1", "b_t1", "w_t2", "b_t2", "w_m", "b_m", "mod_out", "ws"};
+  for (int i = 0; i < 8; ++i) ARDIT_TRY(check_ptr(p[i], n[i]));
+  const Ws L = ws_layout(dims, n_streams, 0, 0);
+  if (ws_bytes < L.h) return fail(ARDIT_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.h);
+  const int D = dims->dim;
+  float* s = at<float>(ws, L.tsin);
+  float* e1 = at<float>(ws, L.te1);
+  float* e2 = at<float>(ws, L.te2);
+  auto B16 = [](const void* q) { return static_cast<const bf16_t*>(q); };
+  ARDIT_HIP(launch_time_sinusoid(stream, t_host, n_streams, s), "time sinusoid");
+  ARDIT_HIP(launch_linear_small(stream, s, n_streams, ARDIT_TIME_FREQ_DIM, B16(tw->w_t1),
+                                B16(tw->b_t1), D, e1, false), "time mlp 1");
+  ARDIT_HIP(launch_linear_small(stream, e1, n_streams, D, B16(tw->w_t2), B16(tw->b_t2), D, e2,
+                                true), "time mlp 2");
+  ARDIT_HIP(launch_linear_small(stream, e2, n_streams, D, B16(tw->w_m), B16(tw->b_m), 6 * D,
+                                mod_out, true), "time modulation");
+  return ARDIT_OK;
+}
+
+int ardit_ctx_kv(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                 const void* ctx, const ardit_block_weights* w, void* ctx_k, void* ctx_v,
+                 void* ws, size_t ws_bytes) {
+  ARDIT_TRY(check_dims(dims));
+  ARDIT_TRY(check_batch(dims, batch, kUseCtx));
+  ARDIT_TRY(check_ptr(ctx, "ctx"));
+  ARDIT_TRY(check_ptr(ctx_k, "ctx_k"));
+  ARDIT_TRY(check_ptr(ctx_v, "ctx_v"));
+  ARDIT_TRY(check_block_weights(w, true));
+  ardit_batch cb = *batch;
+  cb.q_lens = nullptr;
+  Ws L;
+  ARDIT_TRY(check_ws(dims, &cb, ws, ws_bytes, &L));
+  const int Nc = static_cast<int>(sum_ctx(batch));
+  const int D = dims->dim;
+  bf16_t* ck = at<bf16_t>(ws, L.ck);
+  bf16_t* cv = at<bf16_t>(ws, L.cv);
+  const RowStreams rs = ctx_streams(batch);
+  auto B16 = [](const void* q) { return static_cast<const bf16_t*>(q); };
+  GemmEpiArgs e;
+  e.bias = B16(w->b_ck);
+  ARDIT_HIP(launch_gemm(stream, kEpiBias, B16(ctx), D, B16(w->w_ck), D, ck, D, Nc, D, D, e),
+            "ctx k gemm");
+  ARDIT_HIP(launch_ctx_k_layout(stream, ck, Nc, D, dims->n_heads, dims->head_dim, B16(w->g_ck),
+                                dims->eps, static_cast<bf16_t*>(ctx_k), rs),
+            "ctx k layout");
+  e.bias = B16(w->b_cv);
+  ARDIT_HIP(launch_gemm(stream, kEpiBias, B16(ctx), D, B16(w->w_cv), D, cv, D, Nc, D, D, e),
+            "ctx v gemm");
+  ARDIT_HIP(launch_v_transpose(stream, cv, D, 0, Nc, D, dims->n_heads, dims->head_dim,
+                               static_cast<bf16_t*>(ctx_v), false, 0, nullptr, 0, 0, rs),
+            "ctx v layout");
+  return ARDIT_OK;
+}
+
+int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                    const void* qkv, const void* g_q, const void* g_k, const ardit_kv_paged* kv,
+                    void* q_out) {
+  ARDIT_TRY(check_dims(dims));
+  ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache | kUsePos | kChunkQ));
+  ARDIT_TRY(check_kv(dims, batch, kv));
+  ARDIT_TRY(check_ptr(qkv, "qkv"));
+  ARDIT_TRY(check_ptr(g_q, "g_q"));
+  ARDIT_TRY(check_ptr(g_k, "g_k"));
+  ARDIT_TRY(check_ptr(q_out, "q_out"));
+  const int N = static_cast<int>(sum_q(batch));
+  const RowStreams rs = q_streams(batch);
+  const int D = dims->dim;
+  RopeGeom rg{D, dims->n_heads, dims->head_dim, tokens_per_frame(dims), dims->lat_w,
+              kv->max_frames, kv->n_pages, dims->eps, dims->rope_theta};
+  ARDIT_HIP(launch_qk_norm_rope(stream, static_cast<const bf16_t*>(qkv), N, rg,
+                                static_cast<const bf16_t*>(g_q), static_cast<const bf16_t*>(g_k),
+                                static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(kv->k_pages),
+                                kv->page_table, rs),
+            "qk_norm_rope");
+  ARDIT_HIP(launch_v_transpose(stream, static_cast<const bf16_t*>(qkv), 3 * D, 2 * D, N, D,
+                               dims->n_heads, dims->head_dim, static_cast<bf16_t*>(kv->v_pages),
+                               true, tokens_per_frame(dims), kv->page_table, kv->max_frames,
+                               kv->n_pages, rs),
+            "v_append");
+  return ARDIT_OK;
+}
+
+int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                   const void* q, const ardit_kv_paged* kv, void* o) {
+  ARDIT_TRY(check_dims(dims));
+  ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
+  ARDIT_TRY(check_kv(dims, batch, kv));
+  ARDIT_TRY(check_ptr(q, "q"));
+  ARDIT_TRY(check_ptr(o, "o"));
+  const AttnArgs a = self_attn_args(dims, batch, q, kv, o);
+  return run_self_attention(stream, a, dims->head_dim);
+}
+
+int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                           const void* x, const ardit_kv_paged* kv, const float* mod,
+                           const void* ctx_k, const void* ctx_v, const ardit_block_weights* w,
+                           void* out, void* ws, size_t ws_bytes) {
+  ARDIT_TRY(check_block_args(dims, batch, x, kv, mod, ctx_k, ctx_v, w, out));
+  Ws L;
+  ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  return block_chain(stream, dims, batch, x, kv, mod, ctx_k, ctx_v, w, out, ws, L);
+}
+
+int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x, ardit_kv_paged kv,
+                    int32_t cache_len, int32_t frame_pos0, const float* mod, const void* ctx_k,
+                    const void* ctx_v, int32_t ctx_len, const ardit_block_weights* w, void* out,
+                    void* ws, size_t ws_bytes) {
+  ARDIT_TRY(check_dims(dims));
+  const int32_t q_len = chunk_tokens(dims);
+  ardit_batch b;
+  b.n_streams = 1;
+  b.q_lens = &q_len;
+  b.cache_lens = &cache_len;
+  b.frame_pos0 = &frame_pos0;
+  b.ctx_lens = &ctx_len;
+  return ardit_block_fwd_varlen(stream, dims, &b, x, &kv, mod, ctx_k, ctx_v, w, out, ws,
+                                ws_bytes);
+}
+
+int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                    int32_t n_layers, const void* x, const ardit_kv_paged* kv, const float* mod,
+                    const void* const* ctx_k, const void* const* ctx_v,
+                    const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes) {
+  if (n_layers < 1) return fail(ARDIT_EINVAL, "n_layers %d must be >= 1", n_layers);
+  if (!kv || !ctx_k || !ctx_v || !w) return fail(ARDIT_EINVAL, "per-layer arrays must be non-NULL");
+  for (int l = 0; l < n_layers; ++l)
+    ARDIT_TRY(check_block_args(dims, batch, x, &kv[l], mod, ctx_k[l], ctx_v[l], &w[l], out));
+  if (x == out) return fail(ARDIT_EINVAL, "stack input and output must differ");
+  Ws L;
+  ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  // layer 0 reads x and writes out; later layers update out in place (a
+  // layer reads its input only before it writes its output)
+  for (int l = 0; l < n_layers; ++l)
+    ARDIT_TRY(block_chain(stream, dims, batch, l == 0 ? x : out, &kv[l], mod, ctx_k[l], ctx_v[l],
+                          &w[l], out, ws, L));
+  return ARDIT_OK;
+}
+
+int ardit_timing_enable(int enable) {
+  Timing& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.enabled = enable != 0;
+  return ARDIT_OK;
+}
+
+int ardit_timing_collect(int32_t* launches, double* total_ms) {
+  if (!launches || !total_ms) return fail(ARDIT_EINVAL, "outputs must be non-NULL");
+  Timing& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  double sum = 0.0;
+  int n = 0;
+  int status = ARDIT_OK;
+  for (auto& pr : t.rec) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(pr.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
+    if (e != hipSuccess && status == ARDIT_OK) status = hip_fail(e, "timing events");
+    sum += ms;
+    ++n;
+    t.pool.push_back(pr.first);
+    t.pool.push_back(pr.second);
+  }
+  t.rec.clear();
+  *launches = n;
+  *total_ms = sum;
+  return status;
+}
+
+}  // extern "C"

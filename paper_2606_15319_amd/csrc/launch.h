@@ -1,0 +1,120 @@
+// Host-side launchers of the gfx950 kernels (internal to libardit).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace ardit {
+
+constexpr int kMaxStreams = 64;
+
+// ---------------------------------------------------------------- GEMM
+enum GemmEpi : int {
+  kEpiBias = 0,         // C = A W^T + b
+  kEpiBiasGelu = 1,     // C = GELU_tanh(A W^T + b)
+  kEpiBiasGateRes = 2,  // C = R + gate[stream(row)] * (A W^T + b)
+  kEpiBiasRes = 3,      // C = R + (A W^T + b)
+};
+
+struct GemmEpiArgs {
+  const bf16_t* bias = nullptr;      // [N]
+  const bf16_t* res = nullptr;       // [M][ldr]
+  int ldr = 0;
+  const float* mod = nullptr;        // [streams][6][dim]
+  const float* mod_table = nullptr;  // [6][dim]
+  int gate_row = 0;
+  int dim = 0;
+  int rows_per_stream = 1;
+};
+
+// C[M][N] (row stride ldc) = epilogue(A[M][K] (lda) * W[N][K]^T (ldw)).
+// Requires N % 128 == 0, K % 64 == 0, 16-byte aligned rows.
+hipError_t launch_gemm(hipStream_t st, int epi, const bf16_t* A, int lda, const bf16_t* W,
+                       int ldw, bf16_t* C, int ldc, int M, int N, int K, const GemmEpiArgs& ep);
+
+// ----------------------------------------------------------- attention
+struct AttnStream {
+  int32_t q_off;       // first row of the stream in q / o
+  int32_t q_len;
+  int32_t kv_len;      // keys [0, kv_len)
+  int32_t item_begin;  // first work item of the stream
+  int32_t n_qtiles;
+  int32_t stream;      // row of the page table (paged) ...
+  int32_t base_off;    // ... or element offset of the stream's keys (contiguous)
+  int32_t T;           // tokens per page (contiguous: kv_len)
+};
+
+struct AttnArgs {
+  const bf16_t* q;
+  int32_t ldq;
+  bf16_t* o;
+  int32_t ldo;
+  const bf16_t* k;
+  const bf16_t* v;
+  const int32_t* page_table;
+  int32_t max_frames;
+  int32_t n_pages;
+  int32_t T;           // page tokens (paged)
+  FastDiv fT;
+  int32_t H;
+  float scale_log2;    // log2(e) / sqrt(d)
+  int32_t n_streams;
+  int32_t total_items;
+  int32_t per_xcd;
+  AttnStream s[kMaxStreams];
+};
+
+// Fills n_qtiles / item_begin / total_items / per_xcd from the streams' lengths,
+// ordering streams by decreasing key count.
+void plan_attention(AttnArgs& a, int head_dim);
+hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, bool paged);
+
+// --------------------------------------------------------- elementwise
+struct RowStream {
+  int32_t row_begin;
+  int32_t len;
+  int32_t cache_len;   // paged: logical slot of the first row
+  int32_t frame_pos0;
+};
+
+struct RowStreams {
+  int32_t n;
+  RowStream s[kMaxStreams];
+};
+
+hipError_t launch_adaln_norm(hipStream_t st, const bf16_t* x, bf16_t* out, int N, int D,
+                             const float* mod, const float* mod_table, int shift_row,
+                             int scale_row, int rows_per_stream, float eps);
+hipError_t launch_rms_gain(hipStream_t st, const bf16_t* in, bf16_t* out, int N, int D,
+                           const bf16_t* gain, float eps);
+
+struct RopeGeom {
+  int D, H, hd, T, lat_w, max_frames, n_pages;
+  float eps, theta;
+};
+hipError_t launch_qk_norm_rope(hipStream_t st, const bf16_t* qkv, int N, const RopeGeom& g,
+                               const bf16_t* g_q, const bf16_t* g_k, bf16_t* q_out,
+                               bf16_t* k_pages, const int32_t* page_table, const RowStreams& rs);
+
+// Writes rows of src (columns [col_off + h*hd, +hd) per head) into transposed
+// value storage [H][hd][T].  paged: slot = cache_len + row - row_begin through
+// the page table; otherwise stream b's block starts at element row_begin * D
+// of dst with T = len.
+hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int col_off,
+                              int N, int D, int H, int hd, bf16_t* dst, bool paged, int T,
+                              const int32_t* page_table, int max_frames, int n_pages,
+                              const RowStreams& rs);
+
+// rms(src row) * gain written as [H][len][hd] per stream (block at row_begin * D).
+hipError_t launch_ctx_k_layout(hipStream_t st, const bf16_t* src, int N, int D, int H, int hd,
+                               const bf16_t* gain, float eps, bf16_t* dst,
+                               const RowStreams& rs);
+
+// y[b][o] = act_out(sum_k act_in(x[b][k]) W[o][k] + bias[o]); x, y fp32; W, bias bf16.
+hipError_t launch_linear_small(hipStream_t st, const float* x, int B, int K, const bf16_t* W,
+                               const bf16_t* bias, int O, float* y, bool silu_in);
+hipError_t launch_time_sinusoid(hipStream_t st, const float* t_host, int B, float* s_out);
+
+}  // namespace ardit

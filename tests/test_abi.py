@@ -1,0 +1,173 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/ardit.h declares, and host validation returns the documented status
+before anything is enqueued (the fake device addresses below are never
+dereferenced because every call fails a host check first)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+A = pytest.importorskip("paper_2606_15319_amd.ardit",
+                        reason="libardit.so not built (python -m paper_2606_15319_amd.build)")
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "ardit.h")
+FAKE = 1 << 20   # 16-byte aligned stand-in address, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ardit_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported():
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert A.has_symbol(n), n
+    assert set(names) == set(A.exported_symbols())
+
+
+def test_status_strings_and_version():
+    for code, name in A.STATUS.items():
+        assert A.ardit_status_str(code) == name
+    assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
+    assert A.ardit_version() == 100
+
+
+def _dims(**kw):
+    d = dict(dim=256, n_heads=4, head_dim=64, ffn_dim=1024, frames_per_chunk=3, lat_h=8, lat_w=8)
+    d.update(kw)
+    return A.make_dims(**d)
+
+
+def _weights():
+    return A.block_weights({k: FAKE for k in A._BLOCK_FIELDS})
+
+
+def _kv(max_frames=9, n_pages=9):
+    return A.kv_paged(FAKE, FAKE, FAKE, n_pages, max_frames)
+
+
+def _status(fn, *args):
+    with pytest.raises(A.ArditError) as e:
+        fn(*args)
+    return e.value.status
+
+
+def _block(dims=None, cache_len=384, pos=6, ctx_len=32, kv=None, ws_bytes=None, x=FAKE, w=None):
+    dims = dims or _dims()
+    b = A.Batch([192], [cache_len], [pos], [ctx_len])
+    need = A.ardit_workspace_size(dims, b) if ws_bytes is None else ws_bytes
+    A.ardit_block_fwd(FAKE, dims, x, kv or _kv(), cache_len, pos, FAKE, FAKE, FAKE, ctx_len,
+                      w or _weights(), FAKE, FAKE, need)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=96, n_heads=2, dim=192), -5),     # head_dim outside {64, 128}
+    (dict(n_heads=3), -2),                           # D != H * d
+    (dict(dim=320, n_heads=5), -5),                  # D not a multiple of 128
+    (dict(ffn_dim=1000), -5),
+    (dict(lat_h=3, lat_w=3), -5),                    # T not a multiple of 8
+    (dict(lat_w=0), -2),
+])
+def test_dims_rejected(kw, code):
+    assert _status(_block, _dims(**kw)) == code
+
+
+def test_cache_len_not_frame_multiple():
+    assert _status(_block, None, 100) == -2
+
+
+def test_cache_overflow_is_capacity():
+    assert _status(_block, None, 384, 6, 32, _kv(max_frames=8)) == -3
+
+
+def test_workspace_too_small():
+    assert _status(_block, None, 384, 6, 32, None, 1024) == -4
+
+
+def test_null_and_misaligned_pointers():
+    assert _status(_block, None, 384, 6, 32, None, None, 0) == -1
+    assert _status(_block, None, 384, 6, 32, None, None, FAKE + 2) == -1
+    w = {k: FAKE for k in A._BLOCK_FIELDS}
+    w["w_o"] = 0
+    assert _status(_block, None, 384, 6, 32, None, None, FAKE, A.block_weights(w)) == -1
+
+
+def test_ctx_len_zero_rejected():
+    assert _status(_block, None, 384, 6, 0) == -2
+
+
+def test_varlen_wrong_chunk_length():
+    d = _dims()
+    b = A.Batch([192, 100], [0, 0], [0, 0], [8, 8])
+    assert _status(A.ardit_block_fwd_varlen, FAKE, d, b, FAKE, _kv(), FAKE, FAKE, FAKE,
+                   _weights(), FAKE, FAKE, 1 << 30) == -2
+
+
+def test_too_many_streams():
+    d = _dims()
+    b = A.Batch([192] * 65, [0] * 65, [0] * 65, [8] * 65)
+    assert _status(A.ardit_workspace_size, d, b) == -1
+
+
+def test_attn_fwd_validation():
+    d = _dims()
+    b = A.Batch([100], [64])
+    assert _status(A.ardit_attn_fwd, FAKE, d, b, FAKE, _kv(max_frames=2), FAKE) == -3
+    assert _status(A.ardit_attn_fwd, FAKE, d, A.Batch([100], [10]), FAKE, _kv(), FAKE) == -2
+
+
+def test_time_mod_validation():
+    d = _dims()
+    tw = A.time_weights({k: FAKE for k in A._TIME_FIELDS})
+    assert _status(A.ardit_time_mod, FAKE, d, [], tw, FAKE, FAKE, 1 << 20) == -1
+    assert _status(A.ardit_time_mod, FAKE, d, [1.0], tw, FAKE, FAKE, 16) == -4
+
+
+def test_stack_rejects_aliasing_and_bad_layers():
+    d = _dims()
+    b = A.Batch([192], [384], [6], [32])
+    need = A.ardit_workspace_size(d, b)
+    assert _status(A.ardit_stack_fwd, FAKE, d, b, FAKE, [], FAKE, [], [], [], FAKE, FAKE,
+                   need) == -1
+    assert _status(A.ardit_stack_fwd, FAKE, d, b, FAKE, [_kv()], FAKE, [FAKE], [FAKE],
+                   [_weights()], FAKE, FAKE, need) == -1
+
+
+def test_workspace_size_grows_with_tokens():
+    d = _dims()
+    s1 = A.ardit_workspace_size(d, A.Batch([192], [0], [0], [32]))
+    s2 = A.ardit_workspace_size(d, A.Batch([192, 192], [0, 0], [0, 0], [32, 32]))
+    assert s2 > s1 > 0 and s1 % 256 == 0
+
+
+def test_last_error_names_the_problem():
+    with pytest.raises(A.ArditError):
+        _block(_dims(n_heads=3))
+    assert "n_heads" in A.ardit_last_error()
+
+
+def test_layout_round_trip():
+    from paper_2606_15319_amd.layout import (pack_pages, unpack_pages, ctx_to_device_layout,
+                                             ctx_from_device_layout)
+    rng = np.random.default_rng(0)
+    H, d, T = 3, 8, 16
+    n = 40
+    k = rng.standard_normal((n, H, d)).astype(np.float32)
+    v = rng.standard_normal((n, H, d)).astype(np.float32)
+    kp = np.zeros((5, H, T, d), np.float32)
+    vp = np.zeros((5, H, d, T), np.float32)
+    ids = [4, 0, 2]
+    pack_pages(k, v, ids, kp, vp)
+    assert kp[4, 1, 3, 5] == k[3, 1, 5] and vp[0, 2, 6, 1] == v[17, 2, 6]
+    k2, v2 = unpack_pages(kp, vp, ids, n)
+    assert np.array_equal(k2, k) and np.array_equal(v2, v)
+    kc = rng.standard_normal((7, H * d))
+    vc = rng.standard_normal((7, H * d))
+    kf, vf = ctx_to_device_layout(kc, vc, H)
+    kc2, vc2 = ctx_from_device_layout(kf, vf, 7, H, d)
+    assert np.array_equal(kc, kc2) and np.array_equal(vc, vc2)
