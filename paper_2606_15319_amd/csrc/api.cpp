@@ -190,8 +190,8 @@ Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc) {
   w.qkv = take(2 * N * 3 * D);
   w.q = take(2 * N * D);
   w.o = take(2 * N * D);
-  w.x1 = take(2 * N * D);
-  w.x2 = take(2 * N * D);
+  w.x1 = take(4 * N * D);   // fp32: the residual stream inside a block stays fp32
+  w.x2 = take(4 * N * D);
   w.u = take(2 * N * F);
   w.ck = take(2 * Nc * D);
   w.cv = take(2 * Nc * D);
@@ -376,8 +376,8 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   bf16_t* qkv = at<bf16_t>(ws, L.qkv);
   bf16_t* q = at<bf16_t>(ws, L.q);
   bf16_t* o = at<bf16_t>(ws, L.o);
-  bf16_t* x1 = at<bf16_t>(ws, L.x1);
-  bf16_t* x2 = at<bf16_t>(ws, L.x2);
+  float* x1 = at<float>(ws, L.x1);
+  float* x2 = at<float>(ws, L.x2);
   bf16_t* u = at<bf16_t>(ws, L.u);
   bf16_t* y = static_cast<bf16_t*>(out);
   const float* mt = w->mod_table;
@@ -385,7 +385,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   auto B16 = [](const void* p) { return static_cast<const bf16_t*>(p); };
 
   // adaLN RMSNorm #1 and the QKV projection
-  ARDIT_HIP(launch_adaln_norm(st, x, h, N, D, mod, mt, 0, 1, Lq, d->eps), "adaln_norm");
+  ARDIT_HIP(launch_adaln_norm(st, x, false, h, N, D, mod, mt, 0, 1, Lq, d->eps), "adaln_norm");
   GemmEpiArgs e;
   e.bias = B16(w->b_qkv);
   ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_qkv), D, qkv, 3 * D, N, 3 * D, D, e),
@@ -413,13 +413,14 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.gate_row = 2;
   e.dim = D;
   e.rows_per_stream = Lq;
+  e.out_f32 = true;
   ARDIT_HIP(launch_gemm(st, kEpiBiasGateRes, o, D, B16(w->w_o), D, x1, D, N, D, D, e), "o gemm");
   // cross-attention query: rms(rms(x1) g_n3 W_cq^T + b_cq) g_cq
-  ARDIT_HIP(launch_rms_gain(st, x1, h, N, D, B16(w->g_n3), d->eps), "cross pre-norm");
+  ARDIT_HIP(launch_rms_gain(st, x1, true, h, N, D, B16(w->g_n3), d->eps), "cross pre-norm");
   e = GemmEpiArgs();
   e.bias = B16(w->b_cq);
   ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_cq), D, q, D, N, D, D, e), "cq gemm");
-  ARDIT_HIP(launch_rms_gain(st, q, q, N, D, B16(w->g_cq), d->eps), "cross q-norm");
+  ARDIT_HIP(launch_rms_gain(st, q, false, q, N, D, B16(w->g_cq), d->eps), "cross q-norm");
   const AttnArgs ca = cross_attn_args(d, b, q, ctx_k, ctx_v, o);
   ARDIT_HIP(launch_attention(st, ca, hd, false), "cross-attention");
   // x2 = x1 + o_c W_co^T + b_co
@@ -427,9 +428,11 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.bias = B16(w->b_co);
   e.res = x1;
   e.ldr = D;
+  e.res_f32 = true;
+  e.out_f32 = true;
   ARDIT_HIP(launch_gemm(st, kEpiBiasRes, o, D, B16(w->w_co), D, x2, D, N, D, D, e), "co gemm");
   // FFN: out = x2 + gate2 * (GELU(adaLN2(x2) W_1^T + b_1) W_2^T + b_2)
-  ARDIT_HIP(launch_adaln_norm(st, x2, h, N, D, mod, mt, 3, 4, Lq, d->eps), "adaln_norm 2");
+  ARDIT_HIP(launch_adaln_norm(st, x2, true, h, N, D, mod, mt, 3, 4, Lq, d->eps), "adaln_norm 2");
   e = GemmEpiArgs();
   e.bias = B16(w->b_1);
   ARDIT_HIP(launch_gemm(st, kEpiBiasGelu, h, D, B16(w->w_1), D, u, F, N, F, D, e), "ffn up");
@@ -437,6 +440,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.bias = B16(w->b_2);
   e.res = x2;
   e.ldr = D;
+  e.res_f32 = true;
   e.mod = mod;
   e.mod_table = mt;
   e.gate_row = 5;

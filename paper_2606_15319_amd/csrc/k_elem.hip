@@ -14,8 +14,21 @@ namespace ardit {
 constexpr int kMaxChunksPerLane = 16;  // 16 * 8 * 64 = 8192 elements per row
 
 // ------------------------------------------------------------------ norms
+// 8 consecutive elements of a bf16 or fp32 row as fp32
+__device__ __forceinline__ void load8(const bf16_t* p, float* f) {
+  unpack8(*reinterpret_cast<const uint4*>(p), f);
+}
+__device__ __forceinline__ void load8(const float* p, float* f) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+  f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+}
+
+// One wave per row; a lane holds chunks lane + 64 i (i < MAXC) of 8 elements.
+template <typename T, int MAXC>
 __global__ __launch_bounds__(256) void adaln_norm_kernel(
-    const bf16_t* __restrict__ x, bf16_t* __restrict__ out, int N, int D,
+    const T* __restrict__ x, bf16_t* __restrict__ out, int N, int D,
     const float* __restrict__ mod, const float* __restrict__ mod_table, int shift_row,
     int scale_row, int rows_per_stream, float eps) {
   const int lane = threadIdx.x & 63;
@@ -23,18 +36,16 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
   if (row >= N) return;
   const int b = row / rows_per_stream;
   const int nchunk = D >> 3;
-  const uint4* xr = reinterpret_cast<const uint4*>(x + static_cast<size_t>(row) * D);
-  uint4 raw[kMaxChunksPerLane];
+  const T* xr = x + static_cast<size_t>(row) * D;
+  float v[MAXC][8];
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxChunksPerLane; ++i) {
+  for (int i = 0; i < MAXC; ++i) {
     const int c = lane + 64 * i;
     if (c < nchunk) {
-      raw[i] = xr[c];
-      float f[8];
-      unpack8(raw[i], f);
+      load8(xr + 8 * c, v[i]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss += f[e] * f[e];
+      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
     }
   }
   ss = wave_sum(ss);
@@ -45,81 +56,100 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
   const float* tsc = mod_table + static_cast<size_t>(scale_row) * D;
   uint4* orow = reinterpret_cast<uint4*>(out + static_cast<size_t>(row) * D);
 #pragma unroll
-  for (int i = 0; i < kMaxChunksPerLane; ++i) {
+  for (int i = 0; i < MAXC; ++i) {
     const int c = lane + 64 * i;
     if (c < nchunk) {
-      float f[8], y[8];
-      unpack8(raw[i], f);
-      const float4* a0 = reinterpret_cast<const float4*>(msh + 8 * c);
-      const float4* a1 = reinterpret_cast<const float4*>(msc + 8 * c);
-      const float4* b0 = reinterpret_cast<const float4*>(tsh + 8 * c);
-      const float4* b1 = reinterpret_cast<const float4*>(tsc + 8 * c);
-      const float4 sh0 = a0[0], sh1 = a0[1], sc0 = a1[0], sc1 = a1[1];
-      const float4 th0 = b0[0], th1 = b0[1], tc0 = b1[0], tc1 = b1[1];
-      const float shv[8] = {sh0.x + th0.x, sh0.y + th0.y, sh0.z + th0.z, sh0.w + th0.w,
-                            sh1.x + th1.x, sh1.y + th1.y, sh1.z + th1.z, sh1.w + th1.w};
-      const float scv[8] = {sc0.x + tc0.x, sc0.y + tc0.y, sc0.z + tc0.z, sc0.w + tc0.w,
-                            sc1.x + tc1.x, sc1.y + tc1.y, sc1.z + tc1.z, sc1.w + tc1.w};
+      float sh[8], sc[8], th[8], tc[8], y[8];
+      load8(msh + 8 * c, sh);
+      load8(msc + 8 * c, sc);
+      load8(tsh + 8 * c, th);
+      load8(tsc + 8 * c, tc);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = f[e] * r * (1.0f + scv[e]) + shv[e];
+      for (int e = 0; e < 8; ++e) y[e] = v[i][e] * r * (1.0f + sc[e] + tc[e]) + (sh[e] + th[e]);
       orow[c] = pack8(y);
     }
   }
 }
 
-__global__ __launch_bounds__(256) void rms_gain_kernel(const bf16_t* in, bf16_t* out, int N,
-                                                        int D, const bf16_t* __restrict__ gain,
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void rms_gain_kernel(const T* in, bf16_t* out, int N, int D,
+                                                        const bf16_t* __restrict__ gain,
                                                         float eps) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= N) return;
   const int nchunk = D >> 3;
-  const uint4* xr = reinterpret_cast<const uint4*>(in + static_cast<size_t>(row) * D);
-  const uint4* gr = reinterpret_cast<const uint4*>(gain);
-  uint4 raw[kMaxChunksPerLane];
+  const T* xr = in + static_cast<size_t>(row) * D;
+  float v[MAXC][8];
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxChunksPerLane; ++i) {
+  for (int i = 0; i < MAXC; ++i) {
     const int c = lane + 64 * i;
     if (c < nchunk) {
-      raw[i] = xr[c];
-      float f[8];
-      unpack8(raw[i], f);
+      load8(xr + 8 * c, v[i]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss += f[e] * f[e];
+      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
     }
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
   uint4* orow = reinterpret_cast<uint4*>(out + static_cast<size_t>(row) * D);
 #pragma unroll
-  for (int i = 0; i < kMaxChunksPerLane; ++i) {
+  for (int i = 0; i < MAXC; ++i) {
     const int c = lane + 64 * i;
     if (c < nchunk) {
-      float f[8], g[8], y[8];
-      unpack8(raw[i], f);
-      unpack8(gr[c], g);
+      float g[8], y[8];
+      load8(gain + 8 * c, g);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = f[e] * r * g[e];
+      for (int e = 0; e < 8; ++e) y[e] = v[i][e] * r * g[e];
       orow[c] = pack8(y);
     }
   }
 }
 
-hipError_t launch_adaln_norm(hipStream_t st, const bf16_t* x, bf16_t* out, int N, int D,
+// chunks per lane needed for a row of D elements, rounded up to 1, 2, 4, 8, 16
+static int row_chunks(int D) {
+  const int c = (D / 8 + 63) / 64;
+  return c <= 1 ? 1 : c <= 2 ? 2 : c <= 4 ? 4 : c <= 8 ? 8 : 16;
+}
+
+#define ARDIT_ROW_DISPATCH(KERNEL, T, ...)                                              \
+  switch (row_chunks(D)) {                                                              \
+    case 1: hipLaunchKernelGGL((KERNEL<T, 1>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
+    case 2: hipLaunchKernelGGL((KERNEL<T, 2>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
+    case 4: hipLaunchKernelGGL((KERNEL<T, 4>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
+    case 8: hipLaunchKernelGGL((KERNEL<T, 8>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
+    default: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(256), 0, st, __VA_ARGS__); break; \
+  }
+
+hipError_t launch_adaln_norm(hipStream_t st, const void* x, bool x_f32, bf16_t* out, int N, int D,
                              const float* mod, const float* mod_table, int shift_row,
                              int scale_row, int rows_per_stream, float eps) {
   if (N == 0) return hipSuccess;
-  hipLaunchKernelGGL(adaln_norm_kernel, dim3((N + 3) / 4), dim3(256), 0, st, x, out, N, D, mod,
-                     mod_table, shift_row, scale_row, rows_per_stream, eps);
+  const dim3 grid((N + 3) / 4);
+  if (x_f32) {
+    const float* xf = static_cast<const float*>(x);
+    ARDIT_ROW_DISPATCH(adaln_norm_kernel, float, xf, out, N, D, mod, mod_table, shift_row,
+                       scale_row, rows_per_stream, eps);
+  } else {
+    const bf16_t* xb = static_cast<const bf16_t*>(x);
+    ARDIT_ROW_DISPATCH(adaln_norm_kernel, bf16_t, xb, out, N, D, mod, mod_table, shift_row,
+                       scale_row, rows_per_stream, eps);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_rms_gain(hipStream_t st, const bf16_t* in, bf16_t* out, int N, int D,
+hipError_t launch_rms_gain(hipStream_t st, const void* in, bool in_f32, bf16_t* out, int N, int D,
                            const bf16_t* gain, float eps) {
   if (N == 0) return hipSuccess;
-  hipLaunchKernelGGL(rms_gain_kernel, dim3((N + 3) / 4), dim3(256), 0, st, in, out, N, D, gain,
-                     eps);
+  const dim3 grid((N + 3) / 4);
+  if (in_f32) {
+    const float* xf = static_cast<const float*>(in);
+    ARDIT_ROW_DISPATCH(rms_gain_kernel, float, xf, out, N, D, gain, eps);
+  } else {
+    const bf16_t* xb = static_cast<const bf16_t*>(in);
+    ARDIT_ROW_DISPATCH(rms_gain_kernel, bf16_t, xb, out, N, D, gain, eps);
+  }
   return hipGetLastError();
 }
 

@@ -27,10 +27,40 @@ __device__ __forceinline__ bf16x8 lds_frag(const bf16_t* p) {
   return *reinterpret_cast<const bf16x8*>(p);
 }
 
-template <int EPI>
+template <typename T>
+__device__ __forceinline__ void load4(const T* p, float* f);
+template <>
+__device__ __forceinline__ void load4<bf16_t>(const bf16_t* p, float* f) {
+  const uint2 r = *reinterpret_cast<const uint2*>(p);
+  f[0] = __uint_as_float(r.x << 16);
+  f[1] = __uint_as_float(r.x & 0xffff0000u);
+  f[2] = __uint_as_float(r.y << 16);
+  f[3] = __uint_as_float(r.y & 0xffff0000u);
+}
+template <>
+__device__ __forceinline__ void load4<float>(const float* p, float* f) {
+  const float4 r = *reinterpret_cast<const float4*>(p);
+  f[0] = r.x;
+  f[1] = r.y;
+  f[2] = r.z;
+  f[3] = r.w;
+}
+
+__device__ __forceinline__ void store4(bf16_t* p, const float* y) {
+  uint2 out;
+  out.x = pack_bf16x2(y[0], y[1]);
+  out.y = pack_bf16x2(y[2], y[3]);
+  *reinterpret_cast<uint2*>(p) = out;
+}
+__device__ __forceinline__ void store4(float* p, const float* y) {
+  *reinterpret_cast<float4*>(p) = make_float4(y[0], y[1], y[2], y[3]);
+}
+
+// ResT / OutT: element type of the residual input and of C (bf16 or fp32)
+template <int EPI, typename ResT, typename OutT>
 __global__ __launch_bounds__(256, 2) void gemm_kernel(const bf16_t* __restrict__ A, int lda,
                                                       const bf16_t* __restrict__ W, int ldw,
-                                                      bf16_t* __restrict__ C, int ldc, int M,
+                                                      OutT* __restrict__ C, int ldc, int M,
                                                       int N, int K, const GemmEpiArgs ep,
                                                       int tiles_m, int tiles_n, int per_xcd) {
   __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LDS_LD];
@@ -141,9 +171,8 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(const bf16_t* __restrict__
           for (int e = 0; e < 4; ++e) y[e] = gelu_tanh(y[e]);
         }
         if (EPI == kEpiBiasGateRes || EPI == kEpiBiasRes) {
-          const uint2 rr = *reinterpret_cast<const uint2*>(ep.res + static_cast<size_t>(m) * ep.ldr + n0);
-          const float res[4] = {__uint_as_float(rr.x << 16), __uint_as_float(rr.x & 0xffff0000u),
-                                __uint_as_float(rr.y << 16), __uint_as_float(rr.y & 0xffff0000u)};
+          float res[4];
+          load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res);
           if (EPI == kEpiBiasGateRes) {
             const float4 gm4 = *reinterpret_cast<const float4*>(
                 ep.mod + (static_cast<size_t>(sidx) * 6 + ep.gate_row) * ep.dim + n0);
@@ -157,10 +186,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(const bf16_t* __restrict__
             for (int e = 0; e < 4; ++e) y[e] = res[e] + y[e];
           }
         }
-        uint2 out;
-        out.x = pack_bf16x2(y[0], y[1]);
-        out.y = pack_bf16x2(y[2], y[3]);
-        *reinterpret_cast<uint2*>(C + static_cast<size_t>(m) * ldc + n0) = out;
+        store4(C + static_cast<size_t>(m) * ldc + n0, y);
       }
     }
   }
@@ -168,33 +194,46 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(const bf16_t* __restrict__
 
 }  // namespace
 
+template <int EPI, typename ResT, typename OutT>
+static void launch_t(hipStream_t st, const bf16_t* A, int lda, const bf16_t* W, int ldw, void* C,
+                     int ldc, int M, int N, int K, const GemmEpiArgs& ep, int tiles_m,
+                     int tiles_n, int per_xcd) {
+  hipLaunchKernelGGL((gemm_kernel<EPI, ResT, OutT>), dim3(per_xcd * kNumXcd), dim3(256), 0, st,
+                     A, lda, W, ldw, static_cast<OutT*>(C), ldc, M, N, K, ep, tiles_m, tiles_n,
+                     per_xcd);
+}
+
 hipError_t launch_gemm(hipStream_t st, int epi, const bf16_t* A, int lda, const bf16_t* W,
-                       int ldw, bf16_t* C, int ldc, int M, int N, int K, const GemmEpiArgs& ep) {
+                       int ldw, void* C, int ldc, int M, int N, int K, const GemmEpiArgs& ep) {
   if (M == 0) return hipSuccess;
   const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
   const int total = tiles_m * tiles_n;
   const int per_xcd = (total + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(per_xcd * kNumXcd), block(256);
+  const bool rf = ep.res_f32, of = ep.out_f32;
+#define ARDIT_GEMM(E, R, O) launch_t<E, R, O>(st, A, lda, W, ldw, C, ldc, M, N, K, ep, tiles_m, tiles_n, per_xcd)
   switch (epi) {
     case kEpiBias:
-      hipLaunchKernelGGL(gemm_kernel<kEpiBias>, grid, block, 0, st, A, lda, W, ldw, C, ldc, M, N,
-                         K, ep, tiles_m, tiles_n, per_xcd);
+      if (of) ARDIT_GEMM(kEpiBias, bf16_t, float); else ARDIT_GEMM(kEpiBias, bf16_t, bf16_t);
       break;
     case kEpiBiasGelu:
-      hipLaunchKernelGGL(gemm_kernel<kEpiBiasGelu>, grid, block, 0, st, A, lda, W, ldw, C, ldc, M,
-                         N, K, ep, tiles_m, tiles_n, per_xcd);
+      ARDIT_GEMM(kEpiBiasGelu, bf16_t, bf16_t);
       break;
     case kEpiBiasGateRes:
-      hipLaunchKernelGGL(gemm_kernel<kEpiBiasGateRes>, grid, block, 0, st, A, lda, W, ldw, C, ldc,
-                         M, N, K, ep, tiles_m, tiles_n, per_xcd);
+      if (rf && of) ARDIT_GEMM(kEpiBiasGateRes, float, float);
+      else if (rf) ARDIT_GEMM(kEpiBiasGateRes, float, bf16_t);
+      else if (of) ARDIT_GEMM(kEpiBiasGateRes, bf16_t, float);
+      else ARDIT_GEMM(kEpiBiasGateRes, bf16_t, bf16_t);
       break;
     case kEpiBiasRes:
-      hipLaunchKernelGGL(gemm_kernel<kEpiBiasRes>, grid, block, 0, st, A, lda, W, ldw, C, ldc, M,
-                         N, K, ep, tiles_m, tiles_n, per_xcd);
+      if (rf && of) ARDIT_GEMM(kEpiBiasRes, float, float);
+      else if (rf) ARDIT_GEMM(kEpiBiasRes, float, bf16_t);
+      else if (of) ARDIT_GEMM(kEpiBiasRes, bf16_t, float);
+      else ARDIT_GEMM(kEpiBiasRes, bf16_t, bf16_t);
       break;
     default:
       return hipErrorInvalidValue;
   }
+#undef ARDIT_GEMM
   return hipGetLastError();
 }
 

@@ -20,8 +20,10 @@ enum GemmEpi : int {
 
 struct GemmEpiArgs {
   const bf16_t* bias = nullptr;      // [N]
-  const bf16_t* res = nullptr;       // [M][ldr]
+  const void* res = nullptr;         // [M][ldr], bf16 or fp32 (res_f32)
   int ldr = 0;
+  bool res_f32 = false;              // residual stored fp32
+  bool out_f32 = false;              // C stored fp32
   const float* mod = nullptr;        // [streams][6][dim]
   const float* mod_table = nullptr;  // [6][dim]
   int gate_row = 0;
@@ -29,10 +31,10 @@ struct GemmEpiArgs {
   int rows_per_stream = 1;
 };
 
-// C[M][N] (row stride ldc) = epilogue(A[M][K] (lda) * W[N][K]^T (ldw)).
-// Requires N % 128 == 0, K % 64 == 0, 16-byte aligned rows.
+// C[M][N] (row stride ldc, bf16 or fp32 per ep.out_f32) = epilogue(A[M][K] (lda) * W[N][K]^T
+// (ldw)).  Requires N % 128 == 0, K % 64 == 0, 16-byte aligned rows.
 hipError_t launch_gemm(hipStream_t st, int epi, const bf16_t* A, int lda, const bf16_t* W,
-                       int ldw, bf16_t* C, int ldc, int M, int N, int K, const GemmEpiArgs& ep);
+                       int ldw, void* C, int ldc, int M, int N, int K, const GemmEpiArgs& ep);
 
 // ----------------------------------------------------------- attention
 struct AttnStream {
@@ -84,10 +86,11 @@ struct RowStreams {
   RowStream s[kMaxStreams];
 };
 
-hipError_t launch_adaln_norm(hipStream_t st, const bf16_t* x, bf16_t* out, int N, int D,
+// x: bf16 or fp32 rows (x_f32); out: bf16 rows
+hipError_t launch_adaln_norm(hipStream_t st, const void* x, bool x_f32, bf16_t* out, int N, int D,
                              const float* mod, const float* mod_table, int shift_row,
                              int scale_row, int rows_per_stream, float eps);
-hipError_t launch_rms_gain(hipStream_t st, const bf16_t* in, bf16_t* out, int N, int D,
+hipError_t launch_rms_gain(hipStream_t st, const void* in, bool in_f32, bf16_t* out, int N, int D,
                            const bf16_t* gain, float eps);
 
 struct RopeGeom {
