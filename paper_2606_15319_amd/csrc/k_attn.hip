@@ -7,19 +7,23 @@
 // or from one contiguous per-stream block (text cross-attention); both store
 // keys [H][T][d] and values transposed [H][d][T].
 //
-// Work item = (stream, head, 128-query tile); 4 waves x 32 query rows.  Key
-// tiles of 64 are staged in LDS (keys row-major, values d-major), double
-// buffered with register prefetch.  Per wave and tile:
-//   S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (K from LDS, Q held in VGPRs),
+// Work item = (stream, head, 256-query tile); 8 waves x 32 query rows, two
+// waves per SIMD.  Key tiles of 64 are staged in LDS (keys row-major, values
+// d-major), double buffered, with the global loads of tile t+2 issued while
+// tile t is computed (two register sets), and shared by the 8 waves, so each
+// staged byte feeds 256 query rows.  Per wave and tile, on
+// v_mfma_f32_16x16x32_bf16 (each K / V fragment read from LDS feeds the two
+// 16-row query blocks of the wave):
+//   S^T = K Q^T   four 16-key blocks x two query blocks (Q held in VGPRs),
 //   online softmax in fp32 with exp2 (log2(e)/sqrt(d) folded into one FMA),
-//   O^T += V^T P^T on the same MFMA, P taken straight from the S registers.
-// Computing the transposed products puts one query row in each lane, so the
-// row max/sum need only one cross-lane exchange (lanes l and l^32).  The
-// keys of each 32-key block are stored in LDS in the order
-//   kappa(8j + 4g + i) = 16(j/2) + 8g + 4(j%2) + i
-// (j = acc group, g = lane half, i = element), which makes the S values a
-// lane holds for PV step s exactly keys 16s + 8g .. 16s + 8g + 7: the P
-// operand needs no shuffle and the V^T operand is one 16-byte LDS read.
+//   O^T += V^T P^T with P taken straight from the S registers.
+// Computing the transposed products puts one query row in each lane column,
+// so the row max/sum need two cross-lane exchanges (xor 16, xor 32).  Keys of
+// a tile are stored in LDS in the order kappa16 (below), which makes the S
+// values a lane holds for P V step s exactly 8 consecutive keys: the P
+// operand needs no shuffle and the V^T operand is one 16-byte LDS read.  The
+// row sum is accumulated with v_dot2_f32_bf16 on the bf16 P actually fed to
+// the P V product, so numerator and denominator use the same weights.
 #include <math.h>
 
 #include "launch.h"
@@ -28,19 +32,20 @@ namespace ardit {
 
 namespace {
 
-constexpr int BQ = 128;   // queries per work item
+constexpr int BQ = 256;   // queries per work item
 constexpr int BKV = 64;   // keys per tile
 
-// LDS row (within a 32-key block) that holds physical key p
-__device__ __forceinline__ int kappa_inv(int p) {
-  const int a = p >> 4, g = (p >> 3) & 1, b = (p >> 2) & 1, i = p & 3;
-  return 8 * (2 * a + b) + 4 * g + i;
+// Key order of a 64-key tile for 16x16x32 MFMAs: row r of 16-key block kb
+// holds physical key kappa(kb, r) = 32 (kb/2) + 8 (r/4) + 4 (kb%2) + r%4, so
+// the S^T values a lane holds for blocks 2s and 2s+1 are exactly keys
+// 32 s + 8 g .. 32 s + 8 g + 7 (g = lane / 16): the P operand of PV step s.
+__device__ __forceinline__ int kappa16(int kb, int r) {
+  return 32 * (kb >> 1) + 8 * (r >> 2) + 4 * (kb & 1) + (r & 3);
 }
-
-// physical key (within a 32-key block) of MFMA row r
-__device__ __forceinline__ int kappa(int r) {
-  const int j = r >> 3, g = (r >> 2) & 1, i = r & 3;
-  return 16 * (j >> 1) + 8 * g + 4 * (j & 1) + i;
+// LDS row that holds physical key p of the tile
+__device__ __forceinline__ int kappa16_inv(int p) {
+  const int ps = p >> 5, g = (p >> 3) & 3, hh = (p >> 2) & 1, i = p & 3;
+  return 16 * (2 * ps + hh) + 4 * g + i;
 }
 
 // Keys of one 64-key tile: [j0, j0 + 64) starts at offset off0 of page p0 and,
@@ -129,13 +134,13 @@ __device__ __forceinline__ void load_tile(const TileMap& m, int vstride, int j0,
 }
 
 template <int HD, bool PAGED, bool VEC>
-__global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs a) {
+__global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
   constexpr int KLD = HD + 8;          // padded LDS row of the key tile
   constexpr int VLD = BKV + 8;         // padded LDS row of the value tile
-  constexpr int NK = BKV * HD / 8 / 256;   // 16-byte key chunks per thread per tile
-  constexpr int NV = HD * BKV / 8 / 256;   // 16-byte value chunks per thread per tile
-  constexpr int KS = HD / 16;          // MFMA k-steps over d
-  constexpr int DB = HD / 32;          // 32-wide output blocks over d
+  constexpr int NK = BKV * HD / 8 / 512;   // 16-byte key chunks per thread per tile
+  constexpr int NV = HD * BKV / 8 / 512;   // 16-byte value chunks per thread per tile
+  constexpr int KS = HD / 32;          // 16x16x32 MFMA k-steps over d
+  constexpr int DB = HD / 16;          // 16-wide output blocks over d
   __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * KLD];
   __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VLD];
 
@@ -153,15 +158,21 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, g = lane >> 5;
+  const int l16 = lane & 15, g = lane >> 4;
 
-  // ---- Q fragments (B operand of S^T = K Q^T): lane holds row l32, dims 16ks + 8g..
-  const int q_local = qt * BQ + wave * 32 + l32;
-  const int q_row = min(q_local, S.q_len - 1);
-  const bf16_t* qp = a.q + static_cast<size_t>(S.q_off + q_row) * a.ldq + h * HD;
-  bf16x8 qf[KS];
+  // ---- Q fragments (B operand of S^T = K Q^T): the wave's 32 rows are two
+  // 16-row blocks; lane holds row l16 of block qb, dims 32 ks + 8 g ..
+  int q_local[2];
+  bf16x8 qf[2][KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qp + 16 * ks + 8 * g);
+  for (int qb = 0; qb < 2; ++qb) {
+    q_local[qb] = qt * BQ + wave * 32 + 16 * qb + l16;
+    const int q_row = min(q_local[qb], S.q_len - 1);
+    const bf16_t* qp = a.q + static_cast<size_t>(S.q_off + q_row) * a.ldq + h * HD;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[qb][ks] = *reinterpret_cast<const bf16x8*>(qp + 32 * ks + 8 * g);
+  }
 
   const int kv_len = S.kv_len;
   const int vstride = PAGED ? a.T : S.T;   // distance between value dims
@@ -172,135 +183,165 @@ __global__ __launch_bounds__(256, 2) void attn_kernel(const AttnArgs a) {
   int k_row[NK], k_lds[NK];
 #pragma unroll
   for (int i = 0; i < NK; ++i) {
-    const int kr = (tid + 256 * i) / CPR;
+    const int kr = (tid + 512 * i) / CPR;
     k_row[i] = kr;
-    k_lds[i] = ((kr & 32) | kappa_inv(kr & 31)) * KLD + k_cc * 8;
+    k_lds[i] = kappa16_inv(kr) * KLD + k_cc * 8;
   }
   // V chunk i: dim v_dd[i], keys 8 * v_kc .. + 8
   const int v_kc = tid & 7;
   int v_dd[NV];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) v_dd[i] = (tid + 256 * i) >> 3;
+  for (int i = 0; i < NV; ++i) v_dd[i] = (tid + 512 * i) >> 3;
 
-  u32x4 rk[NK], rv[NV];
-  f32x16 o[DB];
+  u32x4 rk[2][NK], rv[2][NV];
+  f32x4 o[2][DB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+  for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
-  float m_run = -INFINITY;   // running max (scaled, log2 units) used for this lane's row
-  float l_run = 0.f;         // this lane's half of the running denominator
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) o[qb][db][v] = 0.f;
+  float m_run[2] = {-INFINITY, -INFINITY};   // running max (scaled, log2) of the lane's rows
+  float l_run[2] = {0.f, 0.f};               // this lane's quarter of each running denominator
   const float c = a.scale_log2;
 
   const int ntiles = (kv_len + BKV - 1) / BKV;
   const int nfull = kv_len / BKV;   // tiles whose 64 keys are all valid
 
-#define ARDIT_LOAD(tile)                                                                   \
+#define ARDIT_LOAD(tile, set)                                                              \
   {                                                                                        \
     const int j0_ = (tile) * BKV;                                                          \
     const TileMap tm_ = map_tile<HD, PAGED>(a, S, h, j0_);                                 \
     if ((tile) < nfull)                                                                    \
-      load_tile<HD, VEC, false>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk, rv); \
+      load_tile<HD, VEC, false>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk[set], rv[set]); \
     else                                                                                   \
-      load_tile<HD, VEC, true>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk, rv);  \
+      load_tile<HD, VEC, true>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk[set], rv[set]);  \
   }
-#define ARDIT_STORE(buf)                                                                   \
+#define ARDIT_STORE(buf, set)                                                              \
   {                                                                                        \
     _Pragma("unroll") for (int i = 0; i < NK; ++i)                                         \
-        *reinterpret_cast<u32x4*>(&sK[buf][k_lds[i]]) = rk[i];                             \
+        *reinterpret_cast<u32x4*>(&sK[buf][k_lds[i]]) = rk[set][i];                        \
     _Pragma("unroll") for (int i = 0; i < NV; ++i)                                         \
-        *reinterpret_cast<u32x4*>(&sV[buf][v_dd[i] * VLD + 8 * v_kc]) = rv[i];             \
+        *reinterpret_cast<u32x4*>(&sV[buf][v_dd[i] * VLD + 8 * v_kc]) = rv[set][i];        \
   }
 
-  ARDIT_LOAD(0);
-  ARDIT_STORE(0);
+  // two tiles of loads in flight: register set (t & 1) holds tile t until stored
+  ARDIT_LOAD(0, 0);
+  if (ntiles > 1) ARDIT_LOAD(1, 1);
+  ARDIT_STORE(0, 0);
   __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) ARDIT_LOAD(t + 1);
-
-    // S^T = K Q^T for the tile's two 32-key blocks
-    f32x16 s[2];
+  for (int t0 = 0; t0 < ntiles; t0 += 2) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int half = 0; half < 2; ++half) {
+    const int t = t0 + half;
+    if (t < ntiles) {
+    const int buf = half;
+    if (t + 2 < ntiles) ARDIT_LOAD(t + 2, half);
+    // S^T = K Q^T: four 16-key blocks x two 16-query blocks, 8 accumulators
+    f32x4 s[4][2];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s[kb][qb][v] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 4; ++kb) {
         const bf16x8 kf =
-            *reinterpret_cast<const bf16x8*>(&sK[buf][(kb * 32 + l32) * KLD + 16 * ks + 8 * g]);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[kb], 0, 0, 0);
+            *reinterpret_cast<const bf16x8*>(&sK[buf][(kb * 16 + l16) * KLD + 32 * ks + 8 * g]);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+          s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][ks], s[kb][qb], 0, 0, 0);
       }
     }
     if (t >= nfull) {   // keys past the end (last tile only)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = t * BKV + kb * 32 + kappa(8 * (v >> 2) + 4 * g + (v & 3));
-          if (key >= kv_len) s[kb][v] = -INFINITY;
+        for (int v = 0; v < 4; ++v) {
+          const int key = t * BKV + kappa16(kb, 4 * g + v);
+          if (key >= kv_len) {
+            s[kb][0][v] = -INFINITY;
+            s[kb][1][v] = -INFINITY;
+          }
         }
     }
     // online softmax in scaled log2 units; the running max is raised only when
     // a row's tile max exceeds it by more than 8 (p <= 2^8 otherwise), so the
     // O / l rescale is skipped on almost every tile
-    float mx = -INFINITY;
+    bf16x8 pf[2][2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int qb = 0; qb < 2; ++qb) {
+      float mx = -INFINITY;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
-    if (__any(mx > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kb][qb][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+      if (__any(mx > m_run[qb] + 8.0f)) {
+        const float m_new = fmaxf(m_run[qb], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-    }
-    bf16x8 pf[4];
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
+          for (int v = 0; v < 4; ++v) o[qb][db][v] *= alpha;
+      }
+      const float mr = m_run[qb];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(s[st >> 1][8 * (st & 1) + e], c, -m_run));
-        l_run += pv;
-        pf[st][e] = static_cast<__bf16>(pv);
+      for (int ps = 0; ps < 2; ++ps) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pv = __builtin_amdgcn_exp2f(fmaf(s[2 * ps + (e >> 2)][qb][e & 3], c, -mr));
+          pf[qb][ps][e] = static_cast<__bf16>(pv);
+        }
+        const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2 pp = {pf[qb][ps][e], pf[qb][ps][e + 1]};
+          l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run[qb], false);
+        }
       }
     }
-    // O^T += V^T P^T
+    // O^T += V^T P^T: 16-dim blocks x two query blocks, 16 accumulators
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
+    for (int ps = 0; ps < 2; ++ps) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const bf16x8 vf =
-            *reinterpret_cast<const bf16x8*>(&sV[buf][(db * 32 + l32) * VLD + 16 * st + 8 * g]);
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st], o[db], 0, 0, 0);
+            *reinterpret_cast<const bf16x8*>(&sV[buf][(db * 16 + l16) * VLD + 32 * ps + 8 * g]);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb][ps], o[qb][db], 0, 0, 0);
       }
     }
-    if (t + 1 < ntiles) ARDIT_STORE(buf ^ 1);
+    if (t + 1 < ntiles) ARDIT_STORE(buf ^ 1, half ^ 1);
     __syncthreads();
+    }
+    }
   }
 #undef ARDIT_LOAD
 #undef ARDIT_STORE
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.0f / l_tot;
-  if (q_local < S.q_len) {
-    bf16_t* op = a.o + static_cast<size_t>(S.q_off + q_local) * a.ldo + h * HD;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+  for (int qb = 0; qb < 2; ++qb) {
+    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float inv = 1.0f / l_tot;
+    if (q_local[qb] < S.q_len) {
+      bf16_t* op = a.o + static_cast<size_t>(S.q_off + q_local[qb]) * a.ldo + h * HD;
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
+      for (int db = 0; db < DB; ++db) {
         uint2 w;
-        w.x = pack_bf16x2(o[db][4 * jj] * inv, o[db][4 * jj + 1] * inv);
-        w.y = pack_bf16x2(o[db][4 * jj + 2] * inv, o[db][4 * jj + 3] * inv);
-        *reinterpret_cast<uint2*>(op + 32 * db + 8 * jj + 4 * g) = w;
+        w.x = pack_bf16x2(o[qb][db][0] * inv, o[qb][db][1] * inv);
+        w.y = pack_bf16x2(o[qb][db][2] * inv, o[qb][db][3] * inv);
+        *reinterpret_cast<uint2*>(op + 16 * db + 4 * g) = w;
       }
+    }
   }
 }
 
@@ -335,7 +376,7 @@ void plan_attention(AttnArgs& a, int /*head_dim*/) {
 
 hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, bool paged) {
   if (a.total_items == 0) return hipSuccess;
-  const dim3 grid(a.per_xcd * kNumXcd), block(256);
+  const dim3 grid(a.per_xcd * kNumXcd), block(512);
   // contiguous keys take the 16-byte value path only when every block length is a multiple of 8
   bool vec = true;
   if (!paged)
