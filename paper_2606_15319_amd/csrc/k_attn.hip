@@ -7,23 +7,19 @@
 // or from one contiguous per-stream block (text cross-attention); both store
 // keys [H][T][d] and values transposed [H][d][T].
 //
-// Work item = (stream, head, 256-query tile); 8 waves x 32 query rows, two
-// waves per SIMD.  Key tiles of 64 are staged in LDS (keys row-major, values
-// d-major), double buffered, with the global loads of tile t+2 issued while
-// tile t is computed (two register sets), and shared by the 8 waves, so each
-// staged byte feeds 256 query rows.  Per wave and tile, on
-// v_mfma_f32_16x16x32_bf16 (each K / V fragment read from LDS feeds the two
-// 16-row query blocks of the wave):
-//   S^T = K Q^T   four 16-key blocks x two query blocks (Q held in VGPRs),
+// Work item = (stream, head, 128-query tile); 4 waves x 32 query rows.  Key
+// tiles of 64 are staged in LDS (keys row-major, values d-major), double
+// buffered with register prefetch.  Per wave and tile:
+//   S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (K from LDS, Q held in VGPRs),
 //   online softmax in fp32 with exp2 (log2(e)/sqrt(d) folded into one FMA),
-//   O^T += V^T P^T with P taken straight from the S registers.
-// Computing the transposed products puts one query row in each lane column,
-// so the row max/sum need two cross-lane exchanges (xor 16, xor 32).  Keys of
-// a tile are stored in LDS in the order kappa16 (below), which makes the S
-// values a lane holds for P V step s exactly 8 consecutive keys: the P
-// operand needs no shuffle and the V^T operand is one 16-byte LDS read.  The
-// row sum is accumulated with v_dot2_f32_bf16 on the bf16 P actually fed to
-// the P V product, so numerator and denominator use the same weights.
+//   O^T += V^T P^T on the same MFMA, P taken straight from the S registers.
+// Computing the transposed products puts one query row in each lane, so the
+// row max/sum need only one cross-lane exchange (lanes l and l^32).  The
+// keys of each 32-key block are stored in LDS in the order
+//   kappa(8j + 4g + i) = 16(j/2) + 8g + 4(j%2) + i
+// (j = acc group, g = lane half, i = element), which makes the S values a
+// lane holds for PV step s exactly keys 16s + 8g .. 16s + 8g + 7: the P
+// operand needs no shuffle and the V^T operand is one 16-byte LDS read.
 #include <math.h>
 
 #include "launch.h"
@@ -133,6 +129,20 @@ __device__ __forceinline__ void load_tile(const TileMap& m, int vstride, int j0,
   }
 }
 
+// Tile inside one page (the common case): uniform bases plus per-lane byte
+// offsets fixed for the whole kernel, so each load is scalar base + 32-bit
+// vector offset with no per-tile address arithmetic.
+template <int NK, int NV>
+__device__ __forceinline__ void load_tile_fast(const char* kb, const char* vb,
+                                               const uint32_t (&k_off)[NK],
+                                               const uint32_t (&v_off)[NV], u32x4 (&rk)[NK],
+                                               u32x4 (&rv)[NV]) {
+#pragma unroll
+  for (int i = 0; i < NK; ++i) rk[i] = *reinterpret_cast<const u32x4*>(kb + k_off[i]);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) rv[i] = *reinterpret_cast<const u32x4*>(vb + v_off[i]);
+}
+
 template <int HD, bool PAGED, bool VEC>
 __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
   constexpr int KLD = HD + 8;          // padded LDS row of the key tile
@@ -194,6 +204,12 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
   for (int i = 0; i < NV; ++i) v_dd[i] = (tid + 512 * i) >> 3;
 
   u32x4 rk[2][NK], rv[2][NV];
+  // byte offsets of this thread's chunks relative to the tile's first key
+  uint32_t k_off[NK], v_off[NV];
+#pragma unroll
+  for (int i = 0; i < NK; ++i) k_off[i] = static_cast<uint32_t>((k_row[i] * HD + k_cc * 8) * 2);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v_off[i] = static_cast<uint32_t>((v_dd[i] * vstride + 8 * v_kc) * 2);
   f32x4 o[2][DB];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb)
@@ -212,7 +228,10 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
   {                                                                                        \
     const int j0_ = (tile) * BKV;                                                          \
     const TileMap tm_ = map_tile<HD, PAGED>(a, S, h, j0_);                                 \
-    if ((tile) < nfull)                                                                    \
+    if ((tile) < nfull && tm_.off0 + BKV <= tm_.T && VEC)                                  \
+      load_tile_fast(reinterpret_cast<const char*>(tm_.k0 + static_cast<size_t>(tm_.off0) * HD), \
+                     reinterpret_cast<const char*>(tm_.v0 + tm_.off0), k_off, v_off, rk[set], rv[set]); \
+    else if ((tile) < nfull)                                                               \
       load_tile<HD, VEC, false>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk[set], rv[set]); \
     else                                                                                   \
       load_tile<HD, VEC, true>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk[set], rv[set]);  \
