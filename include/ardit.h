@@ -172,9 +172,13 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
 
 /* Paged attention alone: o = softmax(q K^T / sqrt(d)) V per stream and head
  * over logical keys [0, cache_len + q_len) of the stream's pages (the chunk's
- * own keys must already be in the pages).  q, o: device bf16 [sum q_lens][H][d]. */
+ * own keys must already be in the pages).  q, o: device bf16 [sum q_lens][H][d].
+ * ws / ws_bytes as for the block calls (ardit_workspace_size of this batch):
+ * when the (stream, head, query tile) items are too few to fill the GPU, their
+ * key ranges are split between workgroups and the partial results combined
+ * through the workspace. */
 int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
-                   const void* q, const ardit_kv_paged* kv, void* o);
+                   const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes);
 
 /* One block, one stream.  x, out: device bf16 [L_q][D] (L_q = frames_per_chunk * T);
  * kv.page_table has one row.  mod: device fp32 [6][D] (from ardit_time_mod).

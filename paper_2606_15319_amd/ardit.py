@@ -87,7 +87,7 @@ _SIGS = {
     "ardit_kv_append": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp, _vp, _vp,
                                   _P(ardit_kv_paged), _vp]),
     "ardit_attn_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
-                                 _P(ardit_kv_paged), _vp]),
+                                 _P(ardit_kv_paged), _vp, _vp, _sz]),
     "ardit_block_fwd": (C.c_int, [_vp, _P(ardit_dims), _vp, ardit_kv_paged, _i32, _i32, _vp,
                                   _vp, _vp, _i32, _P(ardit_block_weights), _vp, _vp, _sz]),
     "ardit_block_fwd_varlen": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
@@ -222,9 +222,9 @@ def ardit_kv_append(stream, dims, batch: Batch, qkv, g_q, g_k, kv: ardit_kv_page
            "ardit_kv_append")
 
 
-def ardit_attn_fwd(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o):
+def ardit_attn_fwd(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o, ws, ws_bytes):
     _check(_lib.ardit_attn_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(q),
-                               C.byref(kv), _ptr(o)), "ardit_attn_fwd")
+                               C.byref(kv), _ptr(o), _ptr(ws), int(ws_bytes)), "ardit_attn_fwd")
 
 
 def ardit_block_fwd(stream, dims, x, kv: ardit_kv_paged, cache_len, frame_pos0, mod, ctx_k,

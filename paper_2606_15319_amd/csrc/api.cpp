@@ -171,6 +171,7 @@ struct Ws {
   size_t tsin, te1, te2;             // fp32 time-MLP scratch
   size_t h, qkv, q, o, x1, x2, u;    // bf16 block activations
   size_t ck, cv;                     // bf16 text projections
+  size_t attn;                       // fp32 partial results of split attention
   size_t total;
 };
 
@@ -195,6 +196,7 @@ Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc) {
   w.u = take(2 * N * F);
   w.ck = take(2 * Nc * D);
   w.cv = take(2 * Nc * D);
+  w.attn = take(attention_split_bytes(d->head_dim));
   w.total = off;
   return w;
 }
@@ -301,7 +303,7 @@ int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
 }
 
 AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
-                        const ardit_kv_paged* kv, void* o) {
+                        const ardit_kv_paged* kv, void* o, float* split_ws) {
   AttnArgs a;
   memset(&a, 0, sizeof(a));
   a.q = static_cast<const bf16_t*>(q);
@@ -329,12 +331,12 @@ AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q
     s.T = a.T;
     row += b->q_lens[i];
   }
-  plan_attention(a, d->head_dim);
+  plan_attention(a, d->head_dim, split_ws);
   return a;
 }
 
 AttnArgs cross_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
-                         const void* ctx_k, const void* ctx_v, void* o) {
+                         const void* ctx_k, const void* ctx_v, void* o, float* split_ws) {
   AttnArgs a;
   memset(&a, 0, sizeof(a));
   a.q = static_cast<const bf16_t*>(q);
@@ -360,7 +362,7 @@ AttnArgs cross_attn_args(const ardit_dims* d, const ardit_batch* b, const void* 
     row += b->q_lens[i];
     crow += b->ctx_lens[i];
   }
-  plan_attention(a, d->head_dim);
+  plan_attention(a, d->head_dim, split_ws);
   return a;
 }
 
@@ -401,7 +403,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
                                kv->page_table, kv->max_frames, kv->n_pages, rs),
             "v_append");
   // self-attention over [cache | chunk]
-  const AttnArgs sa = self_attn_args(d, b, q, kv, o);
+  const AttnArgs sa = self_attn_args(d, b, q, kv, o, at<float>(ws, L.attn));
   ARDIT_TRY(run_self_attention(st, sa, hd));
   // x1 = x + gate1 * (o W_o^T + b_o)
   e = GemmEpiArgs();
@@ -421,7 +423,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.bias = B16(w->b_cq);
   ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_cq), D, q, D, N, D, D, e), "cq gemm");
   ARDIT_HIP(launch_rms_gain(st, q, false, q, N, D, B16(w->g_cq), d->eps), "cross q-norm");
-  const AttnArgs ca = cross_attn_args(d, b, q, ctx_k, ctx_v, o);
+  const AttnArgs ca = cross_attn_args(d, b, q, ctx_k, ctx_v, o, at<float>(ws, L.attn));
   ARDIT_HIP(launch_attention(st, ca, hd, false), "cross-attention");
   // x2 = x1 + o_c W_co^T + b_co
   e = GemmEpiArgs();
@@ -485,7 +487,7 @@ const char* ardit_status_str(int s) {
 
 const char* ardit_last_error(void) { return g_last_error.c_str(); }
 
-int ardit_version(void) { return 100; }
+int ardit_version(void) { return 200; }
 
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) {
   ARDIT_TRY(check_dims(dims));
@@ -589,13 +591,15 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
 }
 
 int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
-                   const void* q, const ardit_kv_paged* kv, void* o) {
+                   const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes) {
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
   ARDIT_TRY(check_kv(dims, batch, kv));
   ARDIT_TRY(check_ptr(q, "q"));
   ARDIT_TRY(check_ptr(o, "o"));
-  const AttnArgs a = self_attn_args(dims, batch, q, kv, o);
+  Ws L;
+  ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  const AttnArgs a = self_attn_args(dims, batch, q, kv, o, at<float>(ws, L.attn));
   return run_self_attention(stream, a, dims->head_dim);
 }
 

@@ -7,19 +7,27 @@
 // or from one contiguous per-stream block (text cross-attention); both store
 // keys [H][T][d] and values transposed [H][d][T].
 //
-// Work item = (stream, head, 128-query tile); 4 waves x 32 query rows.  Key
-// tiles of 64 are staged in LDS (keys row-major, values d-major), double
-// buffered with register prefetch.  Per wave and tile:
-//   S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (K from LDS, Q held in VGPRs),
+// Work item = (stream, head, 256-query tile): a 512-thread workgroup, eight
+// waves of 32 query rows.  Key tiles of 64 are staged in LDS (keys row-major,
+// values d-major, 16-byte chunks XOR-swizzled across banks) in two buffers,
+// with the global loads of the next two tiles in flight in registers.  Per
+// wave and tile:
+//   S^T = K Q^T   on v_mfma_f32_16x16x32_bf16 (K from LDS, Q held in VGPRs),
 //   online softmax in fp32 with exp2 (log2(e)/sqrt(d) folded into one FMA),
 //   O^T += V^T P^T on the same MFMA, P taken straight from the S registers.
-// Computing the transposed products puts one query row in each lane, so the
-// row max/sum need only one cross-lane exchange (lanes l and l^32).  The
-// keys of each 32-key block are stored in LDS in the order
-//   kappa(8j + 4g + i) = 16(j/2) + 8g + 4(j%2) + i
-// (j = acc group, g = lane half, i = element), which makes the S values a
-// lane holds for PV step s exactly keys 16s + 8g .. 16s + 8g + 7: the P
-// operand needs no shuffle and the V^T operand is one 16-byte LDS read.
+// Computing the transposed products puts one query row in each lane column,
+// so the row max needs two cross-lane exchanges and no LDS round trip.  The
+// keys of a tile are stored in LDS in the order kappa16 below, which makes
+// the S values a lane holds for PV step s exactly the 8 keys that lane
+// supplies to the P operand: P needs no shuffle and each V^T operand is one
+// 16-byte LDS read.  Fragment reads are issued four ahead of the MFMAs that
+// consume them.
+//
+// When the items are so few that one workgroup per item would leave more than
+// a quarter of the CUs idle, each item keeps the first part of its key range
+// and the idle workgroups share the remaining parts; the pieces leave partial
+// results (unnormalised O, running max and denominator in fp32) that a second
+// kernel merges.
 #include <math.h>
 
 #include "launch.h"
@@ -28,8 +36,10 @@ namespace ardit {
 
 namespace {
 
-constexpr int BQ = 256;   // queries per work item
-constexpr int BKV = 64;   // keys per tile
+constexpr int BQ = 256;        // queries per work item
+constexpr int BKV = 64;        // keys per tile
+constexpr int NTHR = 512;      // threads per workgroup
+constexpr int LDS_AHEAD = 4;   // fragment reads in flight ahead of the MFMAs
 
 // Key order of a 64-key tile for 16x16x32 MFMAs: row r of 16-key block kb
 // holds physical key kappa(kb, r) = 32 (kb/2) + 8 (r/4) + 4 (kb%2) + r%4, so
@@ -43,6 +53,11 @@ __device__ __forceinline__ int kappa16_inv(int p) {
   const int ps = p >> 5, g = (p >> 3) & 3, hh = (p >> 2) & 1, i = p & 3;
   return 16 * (2 * ps + hh) + 4 * g + i;
 }
+// 16-byte chunk c of LDS row r sits at chunk c ^ swz(r): 16 consecutive rows
+// then cover every bank for a fixed c.  Rows of 256 bytes (keys, d = 128) use
+// r % 16, rows of 128 bytes (keys d = 64, values) (r / 2) % 8.
+template <int ROWB>
+__device__ __forceinline__ int swz(int r) { return ROWB == 256 ? (r & 15) : ((r >> 1) & 7); }
 
 // Keys of one 64-key tile: [j0, j0 + 64) starts at offset off0 of page p0 and,
 // when it runs past the page end T, continues at offset 0 of page p1.  T >= 64
@@ -143,12 +158,299 @@ __device__ __forceinline__ void load_tile_fast(const char* kb, const char* vb,
   for (int i = 0; i < NV; ++i) rv[i] = *reinterpret_cast<const u32x4*>(vb + v_off[i]);
 }
 
+// Normalised bf16 output of one item.
+template <int HD>
+__device__ __forceinline__ void store_output(const AttnArgs& a, const AttnStream& S, int h, int qt,
+                                             const f32x4 (&o)[2][HD / 16], const float (&l_run)[2]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float inv = 1.0f / l_tot;
+    const int ql = qt * BQ + wave * 32 + 16 * qb + l16;
+    if (ql < S.q_len) {
+      bf16_t* op = a.o + static_cast<size_t>(S.q_off + ql) * a.ldo + h * HD;
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db) {
+        uint2 w;
+        w.x = pack_bf16x2(o[qb][db][0] * inv, o[qb][db][1] * inv);
+        w.y = pack_bf16x2(o[qb][db][2] * inv, o[qb][db][3] * inv);
+        *reinterpret_cast<uint2*>(op + 16 * db + 4 * g) = w;
+      }
+    }
+  }
+}
+
+// Partial results of a piece of a split item into slot `slot`: fp32 o, running
+// max and denominator per query row of the item.
+template <int HD>
+__device__ __forceinline__ void store_partial(const AttnArgs& a, size_t slot,
+                                              const f32x4 (&o)[2][HD / 16],
+                                              const float (&m_run)[2], const float (&l_run)[2]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    const int row = wave * 32 + 16 * qb + l16;
+    float* po = a.part_o + (slot * BQ + row) * HD;
+#pragma unroll
+    for (int db = 0; db < HD / 16; ++db)
+      *reinterpret_cast<float4*>(po + 16 * db + 4 * g) =
+          make_float4(o[qb][db][0], o[qb][db][1], o[qb][db][2], o[qb][db][3]);
+    if (g == 0) {
+      a.part_ml[slot * 2 * BQ + row] = m_run[qb];
+      a.part_ml[slot * 2 * BQ + BQ + row] = l_tot;
+    }
+  }
+}
+
+// Runs key tiles [tb, te) of item (S, head h, query tile qt) over the
+// workgroup's 256 queries, then writes the normalised output (slot < 0) or
+// the partial results into slot `slot`.
 template <int HD, bool PAGED, bool VEC>
-__global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
-  constexpr int KLD = HD + 8;          // padded LDS row of the key tile
-  constexpr int VLD = BKV + 8;         // padded LDS row of the value tile
-  constexpr int NK = BKV * HD / 8 / 512;   // 16-byte key chunks per thread per tile
-  constexpr int NV = HD * BKV / 8 / 512;   // 16-byte value chunks per thread per tile
+__device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& S, int h, int qt,
+                                           int tb, int te, bf16_t (&sK)[2][BKV * HD],
+                                           bf16_t (&sV)[2][HD * BKV], int64_t slot) {
+  constexpr int KLD = HD;              // LDS row of the key tile
+  constexpr int VLD = BKV;             // LDS row of the value tile
+  constexpr int NK = BKV * HD / 8 / NTHR;   // 16-byte key chunks per thread per tile
+  constexpr int NV = HD * BKV / 8 / NTHR;   // 16-byte value chunks per thread per tile
+  constexpr int KS = HD / 32;          // 16x16x32 MFMA k-steps over d
+  constexpr int DB = HD / 16;          // 16-wide output blocks over d
+  static_assert(NK >= 1 && NV >= 1 && 4 * KS > LDS_AHEAD && 2 * DB > LDS_AHEAD, "tile shape");
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+
+  // K chunk i of this thread: key row k_row[i], 16-byte column k_cc
+  constexpr int CPR = HD / 8;
+  const int k_cc = tid % CPR;
+  int k_row[NK], k_lds[NK];
+#pragma unroll
+  for (int i = 0; i < NK; ++i) {
+    const int kr = (tid + NTHR * i) / CPR;
+    k_row[i] = kr;
+    const int R = kappa16_inv(kr);
+    k_lds[i] = R * KLD + 8 * (k_cc ^ swz<HD * 2>(R));
+  }
+  // V chunk i: dim v_dd[i], keys 8 * v_kc .. + 8
+  const int v_kc = tid & 7;
+  int v_dd[NV], v_lds[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    v_dd[i] = (tid + NTHR * i) >> 3;
+    v_lds[i] = v_dd[i] * VLD + 8 * (v_kc ^ swz<BKV * 2>(v_dd[i]));
+  }
+  // fragment read offsets: rows kb * 16 + l16 / db * 16 + l16 share the swizzle of l16
+  int k_frag[KS], v_frag[2];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) k_frag[ks] = l16 * KLD + 8 * ((4 * ks + g) ^ swz<HD * 2>(l16));
+#pragma unroll
+  for (int ps = 0; ps < 2; ++ps) v_frag[ps] = l16 * VLD + 8 * ((4 * ps + g) ^ swz<BKV * 2>(l16));
+  const float c = a.scale_log2;
+
+  // ---- Q fragments (B operand of S^T = K Q^T): the wave's 32 rows are two
+  // 16-row blocks; lane holds row l16 of block qb, dims 32 ks + 8 g ..
+  bf16x8 qf[2][KS];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int q_row = min(qt * BQ + wave * 32 + 16 * qb + l16, S.q_len - 1);
+    const bf16_t* qp = a.q + static_cast<size_t>(S.q_off + q_row) * a.ldq + h * HD;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[qb][ks] = *reinterpret_cast<const bf16x8*>(qp + 32 * ks + 8 * g);
+  }
+
+  const int kv_len = S.kv_len;
+  const int vstride = PAGED ? a.T : S.T;   // distance between value dims
+
+  u32x4 rk[2][NK], rv[2][NV];
+  // byte offsets of this thread's chunks relative to the tile's first key
+  uint32_t k_off[NK], v_off[NV];
+  f32x4 o[2][DB];
+#pragma unroll
+  for (int i = 0; i < NK; ++i) k_off[i] = static_cast<uint32_t>((k_row[i] * HD + k_cc * 8) * 2);
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    v_off[i] = static_cast<uint32_t>((v_dd[i] * vstride + 8 * v_kc) * 2);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) o[qb][db][v] = 0.f;
+  float m_run[2] = {-INFINITY, -INFINITY};   // running max (scaled, log2) of the lane's rows
+  float l_run[2] = {0.f, 0.f};               // this lane's quarter of each running denominator
+
+  const int nfull = kv_len / BKV;         // tiles whose 64 keys are all valid
+
+#define ARDIT_LOAD(tile, set)                                                              \
+{                                                                                        \
+  const int j0_ = (tile) * BKV;                                                          \
+  const TileMap tm_ = map_tile<HD, PAGED>(a, S, h, j0_);                                 \
+  if ((tile) < nfull && tm_.off0 + BKV <= tm_.T && VEC)                                  \
+    load_tile_fast(reinterpret_cast<const char*>(tm_.k0 + static_cast<size_t>(tm_.off0) * HD), \
+                   reinterpret_cast<const char*>(tm_.v0 + tm_.off0), k_off, v_off, rk[set], rv[set]); \
+  else if ((tile) < nfull)                                                               \
+    load_tile<HD, VEC, false>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk[set], rv[set]); \
+  else                                                                                   \
+    load_tile<HD, VEC, true>(tm_, vstride, j0_, kv_len, k_row, k_cc, v_dd, v_kc, rk[set], rv[set]);  \
+}
+#define ARDIT_STORE(buf, set)                                                              \
+{                                                                                        \
+  _Pragma("unroll") for (int i = 0; i < NK; ++i)                                         \
+      *reinterpret_cast<u32x4*>(&sK[buf][k_lds[i]]) = rk[set][i];                        \
+  _Pragma("unroll") for (int i = 0; i < NV; ++i)                                         \
+      *reinterpret_cast<u32x4*>(&sV[buf][v_lds[i]]) = rv[set][i];                        \
+}
+
+  // two tiles of loads in flight: register set (t - tb) & 1 holds tile t until stored
+  ARDIT_LOAD(tb, 0);
+  if (tb + 1 < te) ARDIT_LOAD(tb + 1, 1);
+  ARDIT_STORE(0, 0);
+  __syncthreads();
+  for (int t0 = tb; t0 < te; t0 += 2) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int t = t0 + half;
+      if (t < te) {
+        const int buf = half;
+        if (t + 2 < te) ARDIT_LOAD(t + 2, half);
+        // S^T = K Q^T: four 16-key blocks x two 16-query blocks, 8 accumulators
+        f32x4 s[4][2];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) s[kb][qb][v] = 0.f;
+        {
+          bf16x8 kf[KS][4];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+              kf[ks][kb] = *reinterpret_cast<const bf16x8*>(&sK[buf][kb * 16 * KLD + k_frag[ks]]);
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+              for (int qb = 0; qb < 2; ++qb)
+                s[kb][qb] =
+                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks][kb], qf[qb][ks], s[kb][qb], 0, 0, 0);
+          // schedule: LDS_AHEAD reads, then one read per pair of MFMAs
+          __builtin_amdgcn_sched_group_barrier(0x100, LDS_AHEAD, 0);
+#pragma unroll
+          for (int i = 0; i < 4 * KS - LDS_AHEAD; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * LDS_AHEAD, 0);
+        }
+        if (t >= nfull) {   // keys past the end (last tile only)
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int key = t * BKV + kappa16(kb, 4 * g + v);
+              if (key >= kv_len) {
+                s[kb][0][v] = -INFINITY;
+                s[kb][1][v] = -INFINITY;
+              }
+            }
+        }
+        // online softmax in scaled log2 units; the running max is raised only when
+        // a row's tile max exceeds it by more than 8 (p <= 2^8 otherwise), so the
+        // O / l rescale is skipped on almost every tile
+        bf16x8 pf[2][2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kb][qb][v]);
+          mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+          mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+          if (__any(mx > m_run[qb] + 8.0f)) {
+            const float m_new = fmaxf(m_run[qb], mx);
+            const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+            m_run[qb] = m_new;
+            l_run[qb] *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int v = 0; v < 4; ++v) o[qb][db][v] *= alpha;
+          }
+          const float mr = m_run[qb];
+#pragma unroll
+          for (int ps = 0; ps < 2; ++ps) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float pv =
+                  __builtin_amdgcn_exp2f(fmaf(s[2 * ps + (e >> 2)][qb][e & 3], c, -mr));
+              pf[qb][ps][e] = static_cast<__bf16>(pv);
+            }
+            const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+              const bf16x2 pp = {pf[qb][ps][e], pf[qb][ps][e + 1]};
+              l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run[qb], false);
+            }
+          }
+        }
+        // O^T += V^T P^T: 16-dim blocks x two query blocks, 16 accumulators
+        {
+          bf16x8 vf[2][DB];
+#pragma unroll
+          for (int ps = 0; ps < 2; ++ps)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+              vf[ps][db] = *reinterpret_cast<const bf16x8*>(&sV[buf][db * 16 * VLD + v_frag[ps]]);
+#pragma unroll
+          for (int ps = 0; ps < 2; ++ps)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+              for (int qb = 0; qb < 2; ++qb)
+                o[qb][db] =
+                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[ps][db], pf[qb][ps], o[qb][db], 0, 0, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, LDS_AHEAD, 0);
+#pragma unroll
+          for (int i = 0; i < 2 * DB - LDS_AHEAD; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2 * LDS_AHEAD, 0);
+        }
+        if (t + 1 < te) ARDIT_STORE(buf ^ 1, half ^ 1);
+        __syncthreads();
+      }
+    }
+  }
+#undef ARDIT_LOAD
+#undef ARDIT_STORE
+  if (slot < 0)
+    store_output<HD>(a, S, h, qt, o, l_run);
+  else
+    store_partial<HD>(a, static_cast<size_t>(slot), o, m_run, l_run);
+}
+
+// One workgroup per item.  The tile loop is the same as attn_range's; it is
+// kept in the kernel itself because routing it through the inlined function
+// changes the register allocation (copies of the output accumulators every
+// tile) and costs about 2% on long key ranges.
+template <int HD, bool PAGED, bool VEC>
+__global__ __launch_bounds__(NTHR, 1) void attn_kernel(const AttnArgs a) {
+  constexpr int KLD = HD;
+  constexpr int VLD = BKV;
+  constexpr int NK = BKV * HD / 8 / NTHR;   // 16-byte key chunks per thread per tile
+  constexpr int NV = HD * BKV / 8 / NTHR;   // 16-byte value chunks per thread per tile
   constexpr int KS = HD / 32;          // 16x16x32 MFMA k-steps over d
   constexpr int DB = HD / 16;          // 16-wide output blocks over d
   __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * KLD];
@@ -193,15 +495,24 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
   int k_row[NK], k_lds[NK];
 #pragma unroll
   for (int i = 0; i < NK; ++i) {
-    const int kr = (tid + 512 * i) / CPR;
+    const int kr = (tid + NTHR * i) / CPR;
     k_row[i] = kr;
-    k_lds[i] = kappa16_inv(kr) * KLD + k_cc * 8;
+    const int R = kappa16_inv(kr);
+    k_lds[i] = R * KLD + 8 * (k_cc ^ swz<HD * 2>(R));
   }
   // V chunk i: dim v_dd[i], keys 8 * v_kc .. + 8
   const int v_kc = tid & 7;
-  int v_dd[NV];
+  int v_dd[NV], v_lds[NV];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) v_dd[i] = (tid + 512 * i) >> 3;
+  for (int i = 0; i < NV; ++i) {
+    v_dd[i] = (tid + NTHR * i) >> 3;
+    v_lds[i] = v_dd[i] * VLD + 8 * (v_kc ^ swz<BKV * 2>(v_dd[i]));
+  }
+  int k_frag[KS], v_frag[2];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) k_frag[ks] = l16 * KLD + 8 * ((4 * ks + g) ^ swz<HD * 2>(l16));
+#pragma unroll
+  for (int ps = 0; ps < 2; ++ps) v_frag[ps] = l16 * VLD + 8 * ((4 * ps + g) ^ swz<BKV * 2>(l16));
 
   u32x4 rk[2][NK], rv[2][NV];
   // byte offsets of this thread's chunks relative to the tile's first key
@@ -241,7 +552,7 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
     _Pragma("unroll") for (int i = 0; i < NK; ++i)                                         \
         *reinterpret_cast<u32x4*>(&sK[buf][k_lds[i]]) = rk[set][i];                        \
     _Pragma("unroll") for (int i = 0; i < NV; ++i)                                         \
-        *reinterpret_cast<u32x4*>(&sV[buf][v_dd[i] * VLD + 8 * v_kc]) = rv[set][i];        \
+        *reinterpret_cast<u32x4*>(&sV[buf][v_lds[i]]) = rv[set][i];                        \
   }
 
   // two tiles of loads in flight: register set (t & 1) holds tile t until stored
@@ -264,16 +575,27 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) s[kb][qb][v] = 0.f;
+    {
+      bf16x8 kf[KS][4];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const bf16x8 kf =
-            *reinterpret_cast<const bf16x8*>(&sK[buf][(kb * 16 + l16) * KLD + 32 * ks + 8 * g]);
+        for (int kb = 0; kb < 4; ++kb)
+          kf[ks][kb] = *reinterpret_cast<const bf16x8*>(&sK[buf][kb * 16 * KLD + k_frag[ks]]);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-          s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qb][ks], s[kb][qb], 0, 0, 0);
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            s[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks][kb], qf[qb][ks], s[kb][qb], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, LDS_AHEAD, 0);
+#pragma unroll
+      for (int i = 0; i < 4 * KS - LDS_AHEAD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * LDS_AHEAD, 0);
     }
     if (t >= nfull) {   // keys past the end (last tile only)
 #pragma unroll
@@ -327,16 +649,27 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
       }
     }
     // O^T += V^T P^T: 16-dim blocks x two query blocks, 16 accumulators
+    {
+      bf16x8 vf[2][DB];
 #pragma unroll
-    for (int ps = 0; ps < 2; ++ps) {
+      for (int ps = 0; ps < 2; ++ps)
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const bf16x8 vf =
-            *reinterpret_cast<const bf16x8*>(&sV[buf][(db * 16 + l16) * VLD + 32 * ps + 8 * g]);
+        for (int db = 0; db < DB; ++db)
+          vf[ps][db] = *reinterpret_cast<const bf16x8*>(&sV[buf][db * 16 * VLD + v_frag[ps]]);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-          o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qb][ps], o[qb][db], 0, 0, 0);
+      for (int ps = 0; ps < 2; ++ps)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            o[qb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[ps][db], pf[qb][ps], o[qb][db], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, LDS_AHEAD, 0);
+#pragma unroll
+      for (int i = 0; i < 2 * DB - LDS_AHEAD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * LDS_AHEAD, 0);
     }
     if (t + 1 < ntiles) ARDIT_STORE(buf ^ 1, half ^ 1);
     __syncthreads();
@@ -364,9 +697,115 @@ __global__ __launch_bounds__(512, 1) void attn_kernel(const AttnArgs a) {
   }
 }
 
+
+// Split schedule: each item runs its first main_tiles tiles in its own
+// workgroup; the remaining workgroups take equal ranges of the concatenated tails.
+template <int HD, bool PAGED, bool VEC>
+__global__ __launch_bounds__(NTHR, 1) void attn_split_kernel(const AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * BKV];
+
+  const int pid = blockIdx.x;
+  const int xcd = pid % kNumXcd, j = pid / kNumXcd;
+
+  // XCD x runs items [pre, pre + nx), then its share of the tail ranges
+  const int ipx = a.total_items / kNumXcd, irem = a.total_items % kNumXcd;
+  const int nx = ipx + (xcd < irem ? 1 : 0);
+  const int pre = xcd * ipx + min(xcd, irem);
+  if (j < nx) {
+    const int gi = pre + j;
+    int si = 0;
+    for (int i = 1; i < a.n_streams; ++i)
+      if (gi >= a.s[i].item_begin) si = i;
+    const AttnStream S = a.s[si];
+    const int item = gi - S.item_begin;
+    const int h = item / S.n_qtiles, qt = item - h * S.n_qtiles;
+    attn_range<HD, PAGED, VEC>(a, S, h, qt, 0, S.main_tiles, sK, sV,
+                               S.main_tiles == S.n_tiles ? -1 : gi);
+    return;
+  }
+  const int r = a.per_xcd * xcd + j - (pre + nx);   // tail range
+  if (r >= a.split_blocks - a.total_items) return;
+  int pos = r * a.split_tiles;
+  const int end = min(pos + a.split_tiles, a.total_tiles);
+  while (pos < end) {
+    int si = 0;
+    for (int i = 1; i < a.n_streams; ++i)
+      if (pos >= a.s[i].tail_begin) si = i;
+    const AttnStream S = a.s[si];
+    const int tl = S.n_tiles - S.main_tiles;
+    const int rel = pos - S.tail_begin;
+    const int item = rel / tl;
+    const int tb = S.main_tiles + (rel - item * tl);
+    const int te = min(S.n_tiles, tb + (end - pos));
+    pos += te - tb;
+    const int h = item / S.n_qtiles, qt = item - h * S.n_qtiles;
+    // piece (range r, item i) -> slot total_items + i + r: items increase within a
+    // range and the next range starts at the last one's last item, so slots differ
+    attn_range<HD, PAGED, VEC>(a, S, h, qt, tb, te, sK, sV,
+                               static_cast<int64_t>(a.total_items) + S.item_begin + item + r);
+  }
+}
+
+// Combines the partial results of the items that a split schedule cut:
+// o = sum_j 2^(m_j - M) O_j / sum_j 2^(m_j - M) l_j, M = max_j m_j, over the
+// item's main part (slot = item) and the pieces of its tail [w0, w1) of the
+// concatenated tails, held by ranges w0 / W .. (w1 - 1) / W (slot
+// total_items + item + range).
+template <int HD>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const AttnArgs a) {
+  constexpr int TPR = HD / 4;          // threads per row, 4 dims each
+  constexpr int RPB = 256 / TPR;       // rows per workgroup
+  const int gi = blockIdx.x / (BQ / RPB);
+  const int row = (blockIdx.x % (BQ / RPB)) * RPB + threadIdx.x / TPR;
+  int si = 0;
+  for (int i = 1; i < a.n_streams; ++i)
+    if (gi >= a.s[i].item_begin) si = i;
+  const AttnStream& S = a.s[si];
+  const int item = gi - S.item_begin;
+  const int tl = S.n_tiles - S.main_tiles;
+  if (tl == 0) return;   // written whole by its main part
+  const int w0 = S.tail_begin + item * tl, w1 = w0 + tl;
+  const int W = a.split_tiles;
+  const int b_lo = w0 / W, b_hi = (w1 - 1) / W;
+  const int h = item / S.n_qtiles;
+  const int qt = item - h * S.n_qtiles;
+  const int d4 = threadIdx.x % TPR;
+  const int ql = qt * BQ + row;
+  if (ql >= S.q_len) return;
+  {
+    float M = a.part_ml[static_cast<size_t>(gi) * 2 * BQ + row];
+    for (int b = b_lo; b <= b_hi; ++b) {
+      const size_t slot = static_cast<size_t>(a.total_items) + gi + b;
+      M = fmaxf(M, a.part_ml[slot * 2 * BQ + row]);
+    }
+    float l = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int b = b_lo - 1; b <= b_hi; ++b) {
+      const size_t slot = b < b_lo ? static_cast<size_t>(gi) : static_cast<size_t>(a.total_items) + gi + b;
+      const float wgt = __builtin_amdgcn_exp2f(a.part_ml[slot * 2 * BQ + row] - M);
+      l += wgt * a.part_ml[slot * 2 * BQ + BQ + row];
+      const float4 p = *reinterpret_cast<const float4*>(a.part_o + (slot * BQ + row) * HD + 4 * d4);
+      acc.x += wgt * p.x;
+      acc.y += wgt * p.y;
+      acc.z += wgt * p.z;
+      acc.w += wgt * p.w;
+    }
+    const float inv = 1.0f / l;
+    uint2 w;
+    w.x = pack_bf16x2(acc.x * inv, acc.y * inv);
+    w.y = pack_bf16x2(acc.z * inv, acc.w * inv);
+    *reinterpret_cast<uint2*>(a.o + static_cast<size_t>(S.q_off + ql) * a.ldo + h * HD + 4 * d4) = w;
+  }
+}
+
 }  // namespace
 
-void plan_attention(AttnArgs& a, int /*head_dim*/) {
+size_t attention_split_bytes(int head_dim) {
+  return static_cast<size_t>(2) * kAttnSplitBlocks * BQ * (head_dim + 2) * sizeof(float);
+}
+
+void plan_attention(AttnArgs& a, int head_dim, float* split_ws) {
   // order streams by decreasing key count so the longest items start first
   AttnStream tmp[kMaxStreams];
   int n = 0;
@@ -382,37 +821,84 @@ void plan_attention(AttnArgs& a, int /*head_dim*/) {
     tmp[j + 1] = x;
   }
   int items = 0;
+  int64_t work = 0;
   for (int i = 0; i < n; ++i) {
     tmp[i].n_qtiles = (tmp[i].q_len + BQ - 1) / BQ;
+    tmp[i].n_tiles = (tmp[i].kv_len + BKV - 1) / BKV;
+    tmp[i].main_tiles = tmp[i].n_tiles;
+    tmp[i].tail_begin = 0;
     tmp[i].item_begin = items;
     items += tmp[i].n_qtiles * a.H;
-    a.s[i] = tmp[i];
+    work += static_cast<int64_t>(tmp[i].n_qtiles) * a.H * tmp[i].n_tiles;
   }
   a.n_streams = n;
   a.total_items = items;
+  a.total_tiles = 0;
+  a.split_blocks = 0;
+  a.split_tiles = 0;
+  a.part_o = nullptr;
+  a.part_ml = nullptr;
   a.per_xcd = (items + kNumXcd - 1) / kNumXcd;
+  // Split when the items fit one round of workgroups but leave more than a
+  // quarter of them idle: every item keeps its first W tiles (W = the even
+  // share of all tiles per workgroup) and the idle workgroups take equal ranges
+  // of the remaining tails.  Items of one head still run their main parts in
+  // step, sharing key tiles through L2.  The tail ranges cost more per tile
+  // (short segments, partial writes, the merge), which outweighs the gain when
+  // few workgroups are idle.
+  const int spare = kAttnSplitBlocks - items;
+  if (split_ws && items > 0 && spare * 4 > kAttnSplitBlocks &&
+      work >= 8 * static_cast<int64_t>(kAttnSplitBlocks) && work < (static_cast<int64_t>(1) << 30)) {
+    const int W = static_cast<int>((work + kAttnSplitBlocks - 1) / kAttnSplitBlocks);
+    int64_t tails = 0;
+    for (int i = 0; i < n; ++i) {
+      tmp[i].main_tiles = min(tmp[i].n_tiles, W);
+      tmp[i].tail_begin = static_cast<int32_t>(tails);
+      tails += static_cast<int64_t>(tmp[i].n_qtiles) * a.H * (tmp[i].n_tiles - tmp[i].main_tiles);
+    }
+    if (tails > 0) {
+      a.split_blocks = kAttnSplitBlocks;
+      a.total_tiles = static_cast<int32_t>(tails);
+      a.split_tiles = static_cast<int32_t>((tails + spare - 1) / spare);
+      a.part_o = split_ws;
+      a.part_ml = split_ws + static_cast<size_t>(2) * kAttnSplitBlocks * BQ * head_dim;
+      a.per_xcd = kAttnSplitBlocks / kNumXcd;
+    } else {
+      for (int i = 0; i < n; ++i) tmp[i].main_tiles = tmp[i].n_tiles;
+    }
+  }
+  for (int i = 0; i < n; ++i) a.s[i] = tmp[i];
+}
+
+template <int HD, bool P, bool V>
+static void launch_attn_t(hipStream_t st, const AttnArgs& a, dim3 grid) {
+  if (a.split_blocks) {
+    hipLaunchKernelGGL((attn_split_kernel<HD, P, V>), grid, dim3(NTHR), 0, st, a);
+    hipLaunchKernelGGL((attn_merge_kernel<HD>), dim3(a.total_items * (BQ / (256 / (HD / 4)))),
+                       dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((attn_kernel<HD, P, V>), grid, dim3(NTHR), 0, st, a);
+  }
 }
 
 hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, bool paged) {
   if (a.total_items == 0) return hipSuccess;
-  const dim3 grid(a.per_xcd * kNumXcd), block(512);
+  const dim3 grid(a.per_xcd * kNumXcd);
   // contiguous keys take the 16-byte value path only when every block length is a multiple of 8
   bool vec = true;
   if (!paged)
     for (int i = 0; i < a.n_streams; ++i) vec = vec && (a.s[i].T % 8 == 0);
-#define ARDIT_ATTN(HD, P, V) hipLaunchKernelGGL((attn_kernel<HD, P, V>), grid, block, 0, st, a)
   if (head_dim == 128) {
-    if (paged) ARDIT_ATTN(128, true, true);
-    else if (vec) ARDIT_ATTN(128, false, true);
-    else ARDIT_ATTN(128, false, false);
+    if (paged) launch_attn_t<128, true, true>(st, a, grid);
+    else if (vec) launch_attn_t<128, false, true>(st, a, grid);
+    else launch_attn_t<128, false, false>(st, a, grid);
   } else if (head_dim == 64) {
-    if (paged) ARDIT_ATTN(64, true, true);
-    else if (vec) ARDIT_ATTN(64, false, true);
-    else ARDIT_ATTN(64, false, false);
+    if (paged) launch_attn_t<64, true, true>(st, a, grid);
+    else if (vec) launch_attn_t<64, false, true>(st, a, grid);
+    else launch_attn_t<64, false, false>(st, a, grid);
   } else {
     return hipErrorInvalidValue;
   }
-#undef ARDIT_ATTN
   return hipGetLastError();
 }
 

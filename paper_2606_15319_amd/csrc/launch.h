@@ -9,6 +9,8 @@
 namespace ardit {
 
 constexpr int kMaxStreams = 64;
+// workgroups of a split attention schedule (one per CU of an MI355X)
+constexpr int kAttnSplitBlocks = 256;
 
 // ---------------------------------------------------------------- GEMM
 enum GemmEpi : int {
@@ -46,6 +48,9 @@ struct AttnStream {
   int32_t stream;      // row of the page table (paged) ...
   int32_t base_off;    // ... or element offset of the stream's keys (contiguous)
   int32_t T;           // tokens per page (contiguous: kv_len)
+  int32_t n_tiles;     // 64-key tiles of kv_len
+  int32_t main_tiles;  // split schedule: tiles [0, main_tiles) run in the item's own workgroup
+  int32_t tail_begin;  // split schedule: first tail tile of the stream's items, concatenated
 };
 
 struct AttnArgs {
@@ -65,12 +70,20 @@ struct AttnArgs {
   int32_t n_streams;
   int32_t total_items;
   int32_t per_xcd;
+  int32_t split_blocks;  // 0: one workgroup per item; else the workgroups of a split schedule
+  int32_t total_tiles;   // split: tail tiles of all items, concatenated
+  int32_t split_tiles;   // split: tail tiles per spare workgroup
+  float* part_o;         // [2 split_blocks][256][d] partial unnormalised outputs
+  float* part_ml;        // [2 split_blocks][2][256] partial running max, denominator
   AttnStream s[kMaxStreams];
 };
 
-// Fills n_qtiles / item_begin / total_items / per_xcd from the streams' lengths,
-// ordering streams by decreasing key count.
-void plan_attention(AttnArgs& a, int head_dim);
+// Device bytes of the partial results of a split schedule.
+size_t attention_split_bytes(int head_dim);
+// Fills the schedule fields from the streams' lengths, ordering streams by
+// decreasing key count.  split_ws (attention_split_bytes, or null to never
+// split) receives the partial results when the items are cut between workgroups.
+void plan_attention(AttnArgs& a, int head_dim, float* split_ws);
 hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, bool paged);
 
 // --------------------------------------------------------- elementwise

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     for code, name in A.STATUS.items():
         assert A.ardit_status_str(code) == name
     assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
-    assert A.ardit_version() == 100
+    assert A.ardit_version() == 200
 
 
 def _dims(**kw):
@@ -117,8 +117,13 @@ def test_too_many_streams():
 def test_attn_fwd_validation():
     d = _dims()
     b = A.Batch([100], [64])
-    assert _status(A.ardit_attn_fwd, FAKE, d, b, FAKE, _kv(max_frames=2), FAKE) == -3
-    assert _status(A.ardit_attn_fwd, FAKE, d, A.Batch([100], [10]), FAKE, _kv(), FAKE) == -2
+    need = A.ardit_workspace_size(d, b)
+    assert _status(A.ardit_attn_fwd, FAKE, d, b, FAKE, _kv(max_frames=2), FAKE, FAKE, need) == -3
+    assert _status(A.ardit_attn_fwd, FAKE, d, A.Batch([100], [10]), FAKE, _kv(), FAKE, FAKE,
+                   need) == -2
+    # the workspace carries the partial results of a split schedule
+    assert _status(A.ardit_attn_fwd, FAKE, d, b, FAKE, _kv(), FAKE, FAKE, need - 1) == -4
+    assert _status(A.ardit_attn_fwd, FAKE, d, b, FAKE, _kv(), FAKE, 0, need) == -1
 
 
 def test_time_mod_validation():

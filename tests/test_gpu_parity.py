@@ -162,12 +162,21 @@ def _attn_case(A, sh, q_lens, caches, seed, shuffle=True, fill_bits=NAN_BITS, qz
     return pc, dims, batch, q, o, qs, ks, vs
 
 
+def _attn(A, dims, batch, q, kv, o):
+    """ardit_attn_fwd with a workspace of the size the library reports."""
+    import torch
+    n = A.ardit_workspace_size(dims, batch)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    A.ardit_attn_fwd(None, dims, batch, q, kv, o, ws, n)
+    return ws
+
+
 @pytest.mark.parametrize("hd", [64, 128])
 def test_attn_ragged_small(A, hd):
     sh = BlockShape(dim=4 * hd, n_heads=4, head_dim=hd, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
     q_lens, caches = [192, 100, 7, 130], [384, 0, 128, 64]
     pc, dims, batch, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 50)
-    A.ardit_attn_fwd(None, dims, batch, q, pc.kv(A), o)
+    _attn(A, dims, batch, q, pc.kv(A), o)
     _sync()
     og = host_f32(o)
     off = 0
@@ -183,7 +192,7 @@ def test_attn_visibility_nan_poison(A):
     sh = TINY
     q_lens, caches = [100, 33], [64, 0]
     pc, dims, batch, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 51, qzero=True)
-    A.ardit_attn_fwd(None, dims, batch, q, pc.kv(A), o)
+    _attn(A, dims, batch, q, pc.kv(A), o)
     _sync()
     og = host_f32(o)
     off = 0
@@ -200,10 +209,29 @@ def test_attn_page_permutation_bit_identical(A):
     outs = []
     for shuffle in (False, True):
         pc, dims, batch, q, o, *_ = _attn_case(A, sh, [192, 50], [320, 128], 52, shuffle=shuffle)
-        A.ardit_attn_fwd(None, dims, batch, q, pc.kv(A), o)
+        _attn(A, dims, batch, q, pc.kv(A), o)
         _sync()
         outs.append(host_bits(o))
     assert np.array_equal(outs[0], outs[1])
+
+
+def test_attn_split_schedule_ragged(A):
+    """Three streams, 8 heads of 64: 144 (stream, head, 256-query) items for
+    256 CUs, so the key ranges are split between workgroups (ranges cross item
+    and stream boundaries) and merged; sampled rows of every stream, including
+    the ragged last query tile."""
+    sh = BlockShape(dim=512, n_heads=8, head_dim=64, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    q_lens, caches = [1500, 700, 2300], [3008, 0, 1216]
+    pc, dims, batch, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 53)
+    _attn(A, dims, batch, q, pc.kv(A), o)
+    _sync()
+    og = host_f32(o)
+    off = 0
+    for b, n in enumerate(q_lens):
+        rows = sample_rows(n, seed=b)
+        ref = O.attention(qs[b][rows], ks[b], vs[b]).reshape(len(rows), -1)
+        parity(og[off:off + n][rows], ref, f"split attn stream {b}", quantum=ref)
+        off += n
 
 
 def test_attn_chunk_over_cache_4680x14040(A):
@@ -224,7 +252,7 @@ def test_attn_chunk_over_cache_4680x14040(A):
     pc.upload()
     qd = dev_bf16(q)
     o = torch.empty_like(qd)
-    A.ardit_attn_fwd(None, A.dims_from_shape(sh), A.Batch([L], [c]), qd, pc.kv(A), o)
+    _attn(A, A.dims_from_shape(sh), A.Batch([L], [c]), qd, pc.kv(A), o)
     _sync()
     rows = sample_rows(L, seed=2)
     ref = O.attention(q[rows].reshape(-1, H, d), k.reshape(-1, H, d), v).reshape(len(rows), D)
@@ -259,6 +287,20 @@ def test_block_tiny(A):
     run.run()
     _sync()
     _check_block(run, 0, tag="tiny")
+
+
+def test_block_half_tile_widths(A):
+    """dim, 3 dim and ffn_dim that are multiples of 128 but not of 256,
+    a chunk of 144 tokens that ends inside a row tile, and two streams."""
+    import dataclasses
+    sh = BlockShape(dim=384, n_heads=3, head_dim=128, ffn_dim=640, frames=3, lat_h=6, lat_w=8)
+    wl = dataclasses.replace(WORKLOADS["tiny"], shape=sh, cache_chunks=(1, 0),
+                             frame_pos0=(3, 0), timesteps=(750, 250), ctx_len=40)
+    run = BlockRun(wl, A, shuffle_pages_seed=5)
+    run.run()
+    _sync()
+    for b in range(2):
+        _check_block(run, b, tag="half-tile")
 
 
 def test_block_tiny_strong_branches(A):
