@@ -11,7 +11,11 @@ normal draws on the device), resident in HBM before timing starts.
 The JSON line also carries the roofline of the dominant kernel (paged
 self-attention: 4 L_q L_k D flops per launch, timed with HIP events around
 each launch on the stream it runs on) and the float64 CPU oracle timed on
-one block step of layer 0 (cpu_baseline)."""
+one block step of layer 0 (cpu_baseline).  roofline.traffic is the HBM bytes
+per attention launch measured with rocprofv3 counters (FETCH_SIZE and
+WRITE_SIZE, FETCH_SIZE scaled by what it reads for a plain copy of known
+size, see --copy-probe), taken from the profile summary under profiles/ when
+that summary was made from the current attention sources, else null."""
 from __future__ import annotations
 
 import argparse
@@ -39,7 +43,52 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--layers", type=int, default=LAYERS)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="only copy MIB MiB on the device 5 times with one kernel (counter calibration)")
     return p.parse_args()
+
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_paged_block13b_hbm_traffic.md")
+ATTN_SOURCES = ("paper_2606_15319_amd/csrc/k_attn.hip", "paper_2606_15319_amd/csrc/launch.h",
+                "paper_2606_15319_amd/csrc/common.h")
+
+
+def attn_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in ATTN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the counter summary, or None when the
+    summary is missing or was made from other attention sources."""
+    try:
+        fields = {}
+        with open(TRAFFIC_SUMMARY) as f:
+            for line in f:
+                if ":" in line and line.startswith("- "):
+                    k, v = line[2:].split(":", 1)
+                    fields[k.strip()] = v.strip().strip("`")
+        if fields.get("attention sources sha256") != attn_source_hash():
+            return None
+        return int(fields["HBM bytes per launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_probe(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.mul(src, 1.0, out=dst)   # one elementwise kernel: reads and writes mib MiB
+    torch.cuda.synchronize()
+    log(f"copied {mib} MiB 5 times ({mib * (1 << 20)} bytes read and written per copy)")
 
 
 class Model:
@@ -150,6 +199,9 @@ def main():
         print("bench.py runs on one GPU only: the block's hot path is a one-GPU kernel "
               "pipeline; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     import torch
     from paper_2606_15319_amd import ardit as A
     from workloads import WORKLOADS
@@ -212,7 +264,7 @@ def main():
                    "ctx_tokens": wl.ctx_len},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "paged self-attention",
+                     "traffic": measured_traffic(), "kernel": "paged self-attention",
                      "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},
         "cpu_baseline": cpu,
     }
