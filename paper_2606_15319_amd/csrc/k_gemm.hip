@@ -1,31 +1,57 @@
 // bf16 GEMM with fp32 accumulation on gfx950 MFMA, C = epilogue(A W^T).
 //
 // A [M][K] and W [N][K] are both K-contiguous (every projection of the block
-// stores its weight [out][in]).  A 256-thread workgroup computes a 128x128
-// tile; each of its four waves owns a 64x64 quarter as 2x2 blocks of
-// v_mfma_f32_32x32x16_bf16.  K advances in steps of 64 through two LDS
-// buffers: the global loads of step k+1 are issued before the MFMAs of step k
-// and stored to the other buffer afterwards, one barrier per step.  LDS rows
-// are padded to 72 elements (144 bytes) so the 16-byte fragment reads of
-// consecutive rows fall on distinct banks.
+// stores its weight [out][in]).  A 512-thread workgroup computes a 128 x 256
+// tile; its eight waves own 64 x 64 pieces (2 x 4) as 4 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16.  K advances in steps of 64 through three LDS
+// stages filled by direct global->LDS loads (global_load_lds_dwordx4): the
+// loads of step k+2 are in flight while step k is multiplied, and the loaded
+// bytes never pass through registers.  The loads are issued from inline asm:
+// the compiler's own form makes every later LDS read wait for all of them,
+// which would leave no load in flight; the kernel waits on the vector-memory
+// counter itself before the barrier that publishes a stage.  Each LDS row
+// is 128 bytes with its eight 16-byte chunks XOR-swizzled by (row / 2) % 8,
+// so the fragment reads of 16 consecutive rows spread over all banks.  The
+// fragments of both 32-wide halves of a step are read up front and the
+// second half's reads are interleaved with the first half's MFMAs.
 //
 // The MFMA computes C^T = W A^T: W rows feed the A operand and A rows the B
-// operand, so each lane ends up owning one output row m and four groups of
-// four consecutive columns n, which the epilogue writes as 8-byte stores
-// after applying bias / GELU / gate * y + residual in fp32.
+// operand, so each lane ends up owning one output row m and four
+// consecutive columns n per block, which the epilogue writes as 8- or
+// 16-byte stores after applying bias / GELU / gate * y + residual in fp32.
+// Rows past M read a clamped row and store nothing; an N ending on a
+// half tile (N % 256 == 128) clamps W rows the same way.
 #include "launch.h"
 
 namespace ardit {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int LDS_LD = BK + 8;     // padded row, elements
-constexpr int GROUP_M = 8;         // m-tiles per raster group (L2 reuse of W columns)
-
-__device__ __forceinline__ bf16x8 lds_frag(const bf16_t* p) {
-  return *reinterpret_cast<const bf16x8*>(p);
+// 16 bytes per lane from src to LDS at lds + 16 * lane (lds must be the same
+// for all lanes of the wave)
+__device__ __forceinline__ void lds_dma16(const void* src, const void* lds) {
+  const uint32_t m = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char*)lds)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(m) : "m0");
 }
+
+constexpr int BM = 128, BN = 256, BK = 64, NT = 512, STAGES = 3;
+constexpr int NWAVES = NT / 64;
+constexpr int WM = 64, WN = 64, MB = WM / 16, NB = WN / 16;
+constexpr int NWN = BN / WN;
+constexpr int ROW_BYTES = BK * 2;
+constexpr int A_BYTES = BM * ROW_BYTES, W_BYTES = BN * ROW_BYTES;
+constexpr int STAGE_BYTES = A_BYTES + W_BYTES;
+// 1 KB (64 lanes x 16 bytes) load instructions per wave per K step
+constexpr int A_INS = A_BYTES / 1024 / NWAVES;
+constexpr int W_INS = W_BYTES / 1024 / NWAVES;
+constexpr int GROUP_M = 8;   // m-tiles per raster group (L2 reuse of W columns)
+
+static_assert(A_INS * NWAVES * 1024 == A_BYTES && W_INS * NWAVES * 1024 == W_BYTES, "");
+static_assert(STAGES * STAGE_BYTES <= 160 * 1024, "LDS");
+
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 template <typename T>
 __device__ __forceinline__ void load4(const T* p, float* f);
@@ -58,13 +84,12 @@ __device__ __forceinline__ void store4(float* p, const float* y) {
 
 // ResT / OutT: element type of the residual input and of C (bf16 or fp32)
 template <int EPI, typename ResT, typename OutT>
-__global__ __launch_bounds__(256, 2) void gemm_kernel(const bf16_t* __restrict__ A, int lda,
-                                                      const bf16_t* __restrict__ W, int ldw,
-                                                      OutT* __restrict__ C, int ldc, int M,
-                                                      int N, int K, const GemmEpiArgs ep,
-                                                      int tiles_m, int tiles_n, int per_xcd) {
-  __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LDS_LD];
-  __shared__ __attribute__((aligned(16))) bf16_t sW[2][BN * LDS_LD];
+__global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ A, int lda,
+                                                     const bf16_t* __restrict__ W, int ldw,
+                                                     OutT* __restrict__ C, int ldc, int M,
+                                                     int N, int K, const GemmEpiArgs ep,
+                                                     int tiles_m, int tiles_n, int per_xcd) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STAGE_BYTES];
 
   // XCD-aware tile order: consecutive logical tiles land on one XCD (shared L2)
   const int p = blockIdx.x;
@@ -76,118 +101,132 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(const bf16_t* __restrict__
   const int tm = g0 + (L % group) % gm;
   const int tn = (L % group) / gm;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, g = lane >> 5;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int wm = wave / NWN, wn = wave % NWN;
 
-  // global -> register staging: 4 chunks of A and 4 of W per thread per step
-  const bf16_t* a_src[4];
-  const bf16_t* w_src[4];
-  int st_off[4];
+  // Load instruction j of this wave fills the 8 LDS rows 8 (wave * INS + j) .. + 7: lane i
+  // writes slot i % 8 of row 8 (...) + i / 8, which holds chunk (i % 8) ^ swz(row).
+  const char* a_src[A_INS];
+  const char* w_src[W_INS];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i;
-    const int r = c >> 3, kc = c & 7;
-    const int am = min(tm * BM + r, M - 1);
-    a_src[i] = A + static_cast<size_t>(am) * lda + kc * 8;
-    w_src[i] = W + static_cast<size_t>(tn * BN + r) * ldw + kc * 8;
-    st_off[i] = r * LDS_LD + kc * 8;
+  for (int j = 0; j < A_INS; ++j) {
+    const int r = 8 * (wave * A_INS + j) + (lane >> 3);
+    const int c = (lane & 7) ^ swz(r);
+    a_src[j] = reinterpret_cast<const char*>(A + static_cast<size_t>(min(tm * BM + r, M - 1)) * lda) + c * 16;
   }
-  u32x4 ra[4], rw[4];
+#pragma unroll
+  for (int j = 0; j < W_INS; ++j) {
+    const int r = 8 * (wave * W_INS + j) + (lane >> 3);
+    const int c = (lane & 7) ^ swz(r);
+    w_src[j] = reinterpret_cast<const char*>(W + static_cast<size_t>(min(tn * BN + r, N - 1)) * ldw) + c * 16;
+  }
+  auto issue = [&](int kt) {
+    unsigned char* st = smem + (kt % STAGES) * STAGE_BYTES;
+    const int koff = kt * ROW_BYTES;
+#pragma unroll
+    for (int j = 0; j < A_INS; ++j)
+      lds_dma16(a_src[j] + koff, st + (wave * A_INS + j) * 1024);
+#pragma unroll
+    for (int j = 0; j < W_INS; ++j)
+      lds_dma16(w_src[j] + koff, st + A_BYTES + (wave * W_INS + j) * 1024);
+  };
 
-  f32x16 acc[2][2];
+  f32x4 acc[MB][NB];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+      for (int v = 0; v < 4; ++v) acc[a][b][v] = 0.f;
 
   const int nk = K / BK;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
-    rw[i] = *reinterpret_cast<const u32x4*>(w_src[i]);
-    *reinterpret_cast<u32x4*>(&sA[0][st_off[i]]) = ra[i];
-    *reinterpret_cast<u32x4*>(&sW[0][st_off[i]]) = rw[i];
+  issue(0);
+  if (nk > 1) {
+    issue(1);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + W_INS));
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)");
   }
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) {
-      const int k0 = (kt + 1) * BK;
+    if (kt + 2 < nk) issue(kt + 2);
+    const unsigned char* st = smem + (kt % STAGES) * STAGE_BYTES;
+    const bf16_t* cA = reinterpret_cast<const bf16_t*>(st);
+    const bf16_t* cW = reinterpret_cast<const bf16_t*>(st + A_BYTES);
+    bf16x8 fa[2][MB], fw[2][NB];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k0);
-        rw[i] = *reinterpret_cast<const u32x4*>(w_src[i] + k0);
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int r = WN * wn + 16 * nb + l16;
+        fw[kk][nb] = *reinterpret_cast<const bf16x8*>(&cW[r * BK + 8 * ((4 * kk + g) ^ swz(r))]);
+      }
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int r = WM * wm + 16 * mb + l16;
+        fa[kk][mb] = *reinterpret_cast<const bf16x8*>(&cA[r * BK + 8 * ((4 * kk + g) ^ swz(r))]);
       }
     }
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 fw[2], fa[2];
+    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        fw[nb] = lds_frag(&sW[buf][(64 * wn + 32 * nb + l32) * LDS_LD + 16 * ks + 8 * g]);
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-        fa[mb] = lds_frag(&sA[buf][(64 * wm + 32 * mb + l32) * LDS_LD + 16 * ks + 8 * g]);
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
           acc[mb][nb] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[nb], fa[mb], acc[mb][nb], 0, 0, 0);
-    }
-    if (kt + 1 < nk) {
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[kk][nb], fa[kk][mb], acc[mb][nb], 0, 0, 0);
+    // schedule: the first half's LDS reads, then each of its MFMAs paired with one
+    // read of the second half
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *reinterpret_cast<u32x4*>(&sA[buf ^ 1][st_off[i]]) = ra[i];
-        *reinterpret_cast<u32x4*>(&sW[buf ^ 1][st_off[i]]) = rw[i];
-      }
+    for (int i = 0; i < MB + NB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+    for (int i = 0; i < MB * NB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i < MB + NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    // step kt+1 must have landed; the loads of step kt+2 may stay in flight
+    if (kt + 2 < nk) {
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + W_INS));
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)");
     }
     __syncthreads();
   }
 
-  // epilogue: lane owns row m, columns n0..n0+3 of each (mb, nb, jj)
+  // epilogue: lane owns row m and columns n0..n0+3 of each (mb, nb)
+  if (tn * BN + WN * wn >= N) return;
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int m = tm * BM + 64 * wm + 32 * mb + l32;
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = tm * BM + WM * wm + 16 * mb + l16;
     if (m >= M) continue;
     const int sidx = (EPI == kEpiBiasGateRes) ? m / ep.rows_per_stream : 0;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
+      const int n0 = tn * BN + WN * wn + 16 * nb + 4 * g;
+      float y[4], bias[4];
+      load4(ep.bias + n0, bias);
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int n0 = tn * BN + 64 * wn + 32 * nb + 8 * jj + 4 * g;
-        float y[4];
-        const uint2 bb = *reinterpret_cast<const uint2*>(ep.bias + n0);
-        const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
-                               __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+      for (int e = 0; e < 4; ++e) y[e] = acc[mb][nb][e] + bias[e];
+      if (EPI == kEpiBiasGelu) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) y[e] = acc[mb][nb][4 * jj + e] + bias[e];
-        if (EPI == kEpiBiasGelu) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) y[e] = gelu_tanh(y[e]);
-        }
-        if (EPI == kEpiBiasGateRes || EPI == kEpiBiasRes) {
-          float res[4];
-          load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res);
-          if (EPI == kEpiBiasGateRes) {
-            const float4 gm4 = *reinterpret_cast<const float4*>(
-                ep.mod + (static_cast<size_t>(sidx) * 6 + ep.gate_row) * ep.dim + n0);
-            const float4 gt4 = *reinterpret_cast<const float4*>(
-                ep.mod_table + static_cast<size_t>(ep.gate_row) * ep.dim + n0);
-            const float gate[4] = {gm4.x + gt4.x, gm4.y + gt4.y, gm4.z + gt4.z, gm4.w + gt4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) y[e] = res[e] + gate[e] * y[e];
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) y[e] = res[e] + y[e];
-          }
-        }
-        store4(C + static_cast<size_t>(m) * ldc + n0, y);
+        for (int e = 0; e < 4; ++e) y[e] = gelu_tanh(y[e]);
       }
+      if (EPI == kEpiBiasGateRes || EPI == kEpiBiasRes) {
+        float res[4];
+        load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res);
+        if (EPI == kEpiBiasGateRes) {
+          float gm4[4], gt4[4];
+          load4(ep.mod + (static_cast<size_t>(sidx) * 6 + ep.gate_row) * ep.dim + n0, gm4);
+          load4(ep.mod_table + static_cast<size_t>(ep.gate_row) * ep.dim + n0, gt4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = res[e] + (gm4[e] + gt4[e]) * y[e];
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = res[e] + y[e];
+        }
+      }
+      store4(C + static_cast<size_t>(m) * ldc + n0, y);
     }
   }
 }
@@ -198,7 +237,7 @@ template <int EPI, typename ResT, typename OutT>
 static void launch_t(hipStream_t st, const bf16_t* A, int lda, const bf16_t* W, int ldw, void* C,
                      int ldc, int M, int N, int K, const GemmEpiArgs& ep, int tiles_m,
                      int tiles_n, int per_xcd) {
-  hipLaunchKernelGGL((gemm_kernel<EPI, ResT, OutT>), dim3(per_xcd * kNumXcd), dim3(256), 0, st,
+  hipLaunchKernelGGL((gemm_kernel<EPI, ResT, OutT>), dim3(per_xcd * kNumXcd), dim3(NT), 0, st,
                      A, lda, W, ldw, static_cast<OutT*>(C), ldc, M, N, K, ep, tiles_m, tiles_n,
                      per_xcd);
 }
@@ -206,7 +245,8 @@ static void launch_t(hipStream_t st, const bf16_t* A, int lda, const bf16_t* W, 
 hipError_t launch_gemm(hipStream_t st, int epi, const bf16_t* A, int lda, const bf16_t* W,
                        int ldw, void* C, int ldc, int M, int N, int K, const GemmEpiArgs& ep) {
   if (M == 0) return hipSuccess;
-  const int tiles_m = (M + BM - 1) / BM, tiles_n = N / BN;
+  if (N % 128 != 0 || K % BK != 0 || K == 0) return hipErrorInvalidValue;
+  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const int total = tiles_m * tiles_n;
   const int per_xcd = (total + kNumXcd - 1) / kNumXcd;
   const bool rf = ep.res_f32, of = ep.out_f32;
