@@ -80,10 +80,13 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
 }
 
 __device__ __forceinline__ float gelu_tanh(float y) {
-  // tanh(z) = 1 - 2 / (exp(2z) + 1); saturates correctly for large |z|
-  const float z = 0.7978845608028654f * (y + 0.044715f * y * y * y);
-  const float t = 1.0f - 2.0f / (__expf(2.0f * z) + 1.0f);
-  return 0.5f * y * (1.0f + t);
+  // 0.5 y (1 + tanh z) = y * sigmoid(2 z) = y / (1 + 2^(-2 z log2(e))),
+  // z = sqrt(2/pi) (y + 0.044715 y^3): one exp2 and one reciprocal; for large
+  // |y| the power goes to 0 or +inf and the result to y or -0
+  constexpr float c1 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+  constexpr float c2 = c1 * 0.044715f;
+  const float u = y * fmaf(c2, y * y, c1);
+  return y * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(u));
 }
 
 }  // namespace ardit
