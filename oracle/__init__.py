@@ -18,3 +18,4 @@ from .ardit_ref import (  # noqa: F401
     rope_inv_freq, chunk_positions, rope3d, attention, time_modulation,
     context_kv, block_forward, full_sequence_forward,
 )
+from . import sparse_ref  # noqa: F401

@@ -36,6 +36,13 @@ def _f(a):
     return np.asarray(a, dtype=DTYPE)
 
 
+def _bf16_round(a):
+    """Round to the nearest bfloat16 (ties to even), returned as float32."""
+    b = np.ascontiguousarray(np.asarray(a, dtype=np.float32)).view(np.uint32)
+    b = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
+    return b.view(np.float32)
+
+
 # --------------------------------------------------------------------------
 # elementary pieces
 # --------------------------------------------------------------------------
@@ -215,7 +222,7 @@ def _after_self_attention(x, o, M, w, shape, ctx_k, ctx_v):
 
 
 def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
-                  w: dict, shape, rows=None):
+                  w: dict, shape, rows=None, rho: float = 0.0, blocks=None):
     """One block on one chunk of one stream.
 
     x: [L_q, D] chunk activations; cache_k / cache_v: [c, H, d] the stream's
@@ -228,6 +235,10 @@ def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
     c + L_q keys.  rows: optional query-row subset; keys and values are always
     computed for the whole chunk, the rest only for these rows.
 
+    rho > 0 (or an explicit blocks [H, n_qblocks, n_keep] list) makes the
+    self-attention block-sparse as sparse_ref defines it; the selection scores
+    the bf16-rounded rotated q and k, the values the kernels store.
+
     Returns a dict with q (rotated, [L_q, H, d]), k_new, v_new ([L_q, H, d]),
     o (self-attention output, [R, D]), x1, qc, oc, x2, u, out ([R, ...])."""
     x = _f(x)
@@ -237,9 +248,17 @@ def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
     K = np.concatenate([_f(cache_k), k], axis=0)
     V = np.concatenate([_f(cache_v), v], axis=0)
     sel = np.arange(x.shape[0]) if rows is None else np.asarray(rows)
-    o = attention(q[sel], K, V).reshape(len(sel), shape.dim)
+    if rho > 0.0 or blocks is not None:
+        from . import sparse_ref
+        if blocks is None:
+            n_k = (K.shape[0] + sparse_ref.K_BLOCK - 1) // sparse_ref.K_BLOCK
+            scores = sparse_ref.block_scores(_bf16_round(q), _bf16_round(K))
+            blocks = sparse_ref.select_blocks(scores, sparse_ref.keep_count(n_k, rho))
+        o = sparse_ref.sparse_attention(q, K, V, blocks, rows=sel).reshape(len(sel), shape.dim)
+    else:
+        o = attention(q[sel], K, V).reshape(len(sel), shape.dim)
     res = _after_self_attention(x[sel], o, M, w, shape, ctx_k, ctx_v)
-    res.update({"q": q, "k_new": k, "v_new": v, "o": o, "rows": sel})
+    res.update({"q": q, "k_new": k, "v_new": v, "o": o, "rows": sel, "blocks": blocks})
     return res
 
 

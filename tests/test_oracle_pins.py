@@ -416,3 +416,139 @@ def test_workloads_respect_paper_settings():
         assert wl.shape.frames == g["frames_per_chunk"]
         assert max(wl.cache_chunks) <= max(g["kv_window_chunks"])
         assert len(set(wl.timesteps)) <= max(g["denoise_steps"])
+
+
+# --------------------------------------------------------------------------
+# block-sparse attention (sparsity knob rho): selection and masked attention
+# --------------------------------------------------------------------------
+S = O.sparse_ref
+
+
+def test_sparse_keep_counts_for_paper_rho_values():
+    with open(os.path.join(GOLDEN, "paper_settings.json")) as f:
+        rhos = json.load(f)["sparsity"]
+    assert rhos == [0.0, 0.6, 0.7, 0.8, 0.9]
+    # ceil((1 - rho) n) by hand: 10 blocks -> 4, 3, 2, 1; 147 -> 58.8, 44.1, 29.4, 14.7
+    # round up; 585 blocks (the 37440 keys of a 7-chunk window) at 0.9 -> 58.5 -> 59
+    expect = {10: [10, 4, 3, 2, 1], 147: [147, 59, 45, 30, 15], 585: [585, 234, 176, 117, 59],
+              1: [1, 1, 1, 1, 1], 100: [100, 40, 30, 20, 10]}
+    for n, row in expect.items():
+        assert [S.keep_count(n, r) for r in rhos] == row
+        # the single-precision values of the same rho give the same counts
+        assert [S.keep_count(n, float(np.float32(r))) for r in rhos] == row
+    assert S.keep_count(0, 0.5) == 0
+
+
+def test_block_score_is_block_mean_of_logits():
+    rng = np.random.default_rng(7)
+    Lq, Lk, H, d, bq, bk = 11, 8, 2, 3, 4, 3      # ragged last blocks on both sides
+    q = rng.standard_normal((Lq, H, d))
+    k = rng.standard_normal((Lk, H, d))
+    sc = S.block_scores(q, k, bq, bk, dtype=np.float64)
+    assert sc.shape == (H, 3, 3)
+    for h in range(H):
+        for i in range(3):
+            for j in range(3):
+                rows = range(i * bq, min(Lq, (i + 1) * bq))
+                cols = range(j * bk, min(Lk, (j + 1) * bk))
+                tot = sum(sum(q[a, h, c] * k[b, h, c] for c in range(d)) for a in rows for b in cols)
+                assert math.isclose(sc[h, i, j], tot / (len(rows) * len(cols)), rel_tol=1e-12,
+                                    abs_tol=1e-12)
+
+
+def test_selection_of_planted_scores_and_ties():
+    # every query is e0; key block j is c_j e0 +- e1, so its score is exactly c_j
+    c = [3.0, -1.0, 5.0, 0.5, 5.0, 2.0]
+    bk, d = 4, 4
+    q = np.zeros((5, 1, d))
+    q[:, 0, 0] = 1.0
+    k = np.zeros((bk * len(c), 1, d))
+    for j, cj in enumerate(c):
+        k[j * bk:(j + 1) * bk, 0, 0] = cj
+        k[j * bk:(j + 1) * bk, 0, 1] = [1.0, -1.0, 2.0, -2.0]
+    sc = S.block_scores(q, k, 8, bk)
+    np.testing.assert_array_equal(sc[0, 0], np.float32(c))
+    assert S.select_blocks(sc, 3)[0, 0].tolist() == [0, 2, 4]
+    assert S.select_blocks(sc, 1)[0, 0].tolist() == [2]           # tie 2 / 4 -> lower index
+    assert S.select_blocks(sc, 5)[0, 0].tolist() == [0, 2, 3, 4, 5]
+    assert S.select_blocks(-sc, 2)[0, 0].tolist() == [1, 3]       # the sign matters
+    nan = sc.copy()
+    nan[0, 0, 2] = np.nan
+    assert S.select_blocks(nan, 2)[0, 0].tolist() == [0, 4]
+
+
+def test_selection_invariances():
+    rng = np.random.default_rng(3)
+    Lq, Lk, H, d, bq, bk = 24, 40, 3, 8, 8, 8
+    q = rng.standard_normal((Lq, H, d))
+    k = rng.standard_normal((Lk, H, d))
+    base = S.select_blocks(S.block_scores(q, k, bq, bk, np.float64), 2)
+    perm_q = np.concatenate([rng.permutation(np.arange(b, b + bq)) for b in range(0, Lq, bq)])
+    perm_k = np.concatenate([rng.permutation(np.arange(b, b + bk)) for b in range(0, Lk, bk)])
+    got = S.select_blocks(S.block_scores(3.7 * q[perm_q], k[perm_k], bq, bk, np.float64), 2)
+    np.testing.assert_array_equal(got, base)
+    # shifting one key block along the query mean moves it to the top
+    qm = q.mean(axis=0)
+    k2 = k.copy()
+    k2[16:24] += 50.0 * qm[None] / np.linalg.norm(qm, axis=-1, keepdims=True)[None]
+    top = S.select_blocks(S.block_scores(q, k2, Lq, bk, np.float64), 1)
+    assert top[:, 0, 0].tolist() == [2, 2, 2]
+
+
+def test_ragged_last_key_block_mean_uses_valid_keys():
+    rng = np.random.default_rng(5)
+    k = rng.standard_normal((2 * 64 + 1, 2, 4))
+    m = S.block_means(k, 64, np.float64)
+    assert m.shape == (3, 2, 4)
+    np.testing.assert_array_equal(m[2], k[128])
+    np.testing.assert_allclose(m[0], k[:64].mean(axis=0), rtol=1e-13)
+
+
+def test_sparse_attention_brute_force():
+    rng = np.random.default_rng(11)
+    Lq, Lk, H, d, bq, bk = 7, 10, 2, 4, 3, 4        # 3 query blocks, 3 key blocks (last of 2)
+    q = rng.standard_normal((Lq, H, d))
+    k = rng.standard_normal((Lk, H, d))
+    v = rng.standard_normal((Lk, H, d))
+    blocks = np.array([[[0, 2], [1, 2], [0, 1]], [[1, 2], [0, 1], [0, 2]]])
+    o = S.sparse_attention(q, k, v, blocks, bq, bk)
+    for h in range(H):
+        for i in range(Lq):
+            keys = [j for j in range(Lk) if j // bk in blocks[h, i // bq]]
+            ref = _bf_attn_row(list(q[i, h]), [list(k[j, h]) for j in keys],
+                               [list(v[j, h]) for j in keys])
+            np.testing.assert_allclose(o[i, h], ref, rtol=1e-12, atol=1e-12)
+    # a subset of rows gives the same rows
+    np.testing.assert_allclose(S.sparse_attention(q, k, v, blocks, bq, bk, rows=[6, 1]),
+                               o[[6, 1]], rtol=0, atol=0)
+
+
+def test_sparse_rho_zero_is_dense_attention():
+    rng = np.random.default_rng(13)
+    q = rng.standard_normal((300, 2, 8))
+    k = rng.standard_normal((200, 2, 8))
+    v = rng.standard_normal((200, 2, 8))
+    o, blocks = S.sparse_self_attention(q, k, v, 0.0)
+    assert blocks.shape == (2, 2, 4) and (blocks == np.arange(4)).all()
+    np.testing.assert_allclose(o, O.attention(q, k, v), rtol=1e-13, atol=1e-13)
+
+
+def test_sparse_block_forward_keeping_every_block_is_dense():
+    w, _ = _tiny_weights(2)
+    rng = np.random.default_rng(17)
+    sh = TINY
+    x = rng.standard_normal((sh.chunk_tokens, sh.dim))
+    ck = rng.standard_normal((8, sh.n_heads, sh.head_dim))
+    cv = rng.standard_normal((8, sh.n_heads, sh.head_dim))
+    m_t = rng.standard_normal((6, sh.dim)) * 0.1
+    ctxk, ctxv = rng.standard_normal((3, sh.dim)), rng.standard_normal((3, sh.dim))
+    dense = O.block_forward(x, ck, cv, 1, m_t, ctxk, ctxv, w, sh)
+    all_blocks = np.zeros((sh.n_heads, 1, 1), dtype=np.int64)   # 8 + 8 keys: one 64-key block
+    sparse = O.block_forward(x, ck, cv, 1, m_t, ctxk, ctxv, w, sh, blocks=all_blocks)
+    np.testing.assert_allclose(sparse["out"], dense["out"], rtol=1e-12, atol=1e-12)
+    # with small blocks a real selection drops keys and changes the output
+    q, K = dense["q"], np.concatenate([ck, dense["k_new"]])
+    V = np.concatenate([cv, dense["v_new"]])
+    o, blocks = S.sparse_self_attention(q, K, V, 0.5, q_block=4, k_block=4)
+    assert blocks.shape == (sh.n_heads, 2, 2)
+    assert not np.allclose(o, O.attention(q, K, V))
