@@ -99,6 +99,8 @@ typedef struct {
   const int32_t* cache_lens;  /* tokens already in the stream's cache; a multiple of T */
   const int32_t* frame_pos0;  /* absolute latent-frame index of the chunk's first frame (RoPE t) */
   const int32_t* ctx_lens;    /* text tokens per stream (>= 1) */
+  const float* sparsity;      /* attention sparsity rho per stream in [0, 1], or NULL for all 0
+                                 (block-sparse self-attention, see ardit_sparse_select) */
 } ardit_batch;
 
 /* Frame-paged KV cache of one layer (device memory). */
@@ -176,11 +178,36 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
  * ws / ws_bytes as for the block calls (ardit_workspace_size of this batch):
  * when the (stream, head, query tile) items are too few to fill the GPU, their
  * key ranges are split between workgroups and the partial results combined
- * through the workspace. */
+ * through the workspace.  When batch->sparsity gives some stream rho > 0 the
+ * attention is block-sparse: each query tile attends only to the keys of the
+ * tiles ardit_sparse_select would list for it (selection and attention both
+ * run in this call, the lists live in the workspace). */
 int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                    const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes);
 
-/* One block, one stream.  x, out: device bf16 [L_q][D] (L_q = frames_per_chunk * T);
+/* Block selection of block-sparse self-attention (paper, Section 2.1: the
+ * sparsity knob rho skips attention blocks a sparse mask leaves out; Section 5
+ * names Light Forcing as the method, whose rule the paper does not give).
+ * The rule computed: an item is (stream b, head h, query tile i of 256 rows of
+ * the chunk); key tile j is 64 logical keys [64 j, 64 j + 64) of the stream's
+ * [cache | chunk] (the last tile may hold fewer).  Its score is
+ * mean(q~ over the tile's rows) . mean(k~ over the key tile), fp32, and the item
+ * keeps the n_keep = min(n, max(1, ceil((1 - rho_b) n - 1e-3))) tiles of
+ * highest score among its n = ceil((cache_len + q_len) / 64), ties to the
+ * lower index; rho_b = 0 keeps every tile.  NaN scores rank as -inf.
+ * q: device bf16 [sum q_lens][H][d] (rotated queries); the stream's keys must be
+ * in the pages.  blocks: device int32, one row of row_stride entries per item,
+ * rows of stream b starting at row H * sum_{b' < b} ceil(q_lens[b'] / 256),
+ * then head-major, then query tile; a row holds its kept tiles ascending,
+ * then -1 up to row_stride.  row_stride must be at least every stream's
+ * n_keep.  Streams with q_len 0 have no rows.  ws / ws_bytes:
+ * ardit_workspace_size of this batch.  Deterministic: the same inputs give the
+ * same lists as the selection inside ardit_attn_fwd and the block calls. */
+int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                        const void* q, const ardit_kv_paged* kv, int32_t* blocks,
+                        int32_t row_stride, void* ws, size_t ws_bytes);
+
+/* One block, one stream (dense self-attention).  x, out: device bf16 [L_q][D] (L_q = frames_per_chunk * T);
  * kv.page_table has one row.  mod: device fp32 [6][D] (from ardit_time_mod).
  * ctx_k / ctx_v from ardit_ctx_kv with ctx_len text tokens.  Writes the
  * chunk's keys/values into slots [cache_len, cache_len + L_q); the caller
@@ -192,7 +219,8 @@ int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x,
 
 /* One block over a ragged batch of streams sharing the weights (one GPU's share
  * of the streams).  x, out: device bf16 [sum q_lens][D]; mod: device fp32
- * [n_streams][6][D]; page_table rows follow the batch order. */
+ * [n_streams][6][D]; page_table rows follow the batch order.  Streams with
+ * batch->sparsity > 0 run block-sparse self-attention (ardit_sparse_select). */
 int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                            const void* x, const ardit_kv_paged* kv, const float* mod,
                            const void* ctx_k, const void* ctx_v, const ardit_block_weights* w,

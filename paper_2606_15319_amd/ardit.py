@@ -51,7 +51,7 @@ class ardit_dims(C.Structure):
 class ardit_batch(C.Structure):
     _fields_ = [("n_streams", C.c_int32), ("q_lens", C.POINTER(C.c_int32)),
                 ("cache_lens", C.POINTER(C.c_int32)), ("frame_pos0", C.POINTER(C.c_int32)),
-                ("ctx_lens", C.POINTER(C.c_int32))]
+                ("ctx_lens", C.POINTER(C.c_int32)), ("sparsity", C.POINTER(C.c_float))]
 
 
 class ardit_kv_paged(C.Structure):
@@ -88,6 +88,8 @@ _SIGS = {
                                   _P(ardit_kv_paged), _vp]),
     "ardit_attn_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
                                  _P(ardit_kv_paged), _vp, _vp, _sz]),
+    "ardit_sparse_select": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
+                                      _P(ardit_kv_paged), _vp, _i32, _vp, _sz]),
     "ardit_block_fwd": (C.c_int, [_vp, _P(ardit_dims), _vp, ardit_kv_paged, _i32, _i32, _vp,
                                   _vp, _vp, _i32, _P(ardit_block_weights), _vp, _vp, _sz]),
     "ardit_block_fwd_varlen": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
@@ -165,7 +167,8 @@ def dims_from_shape(shape) -> ardit_dims:
 class Batch:
     """Host-side batch descriptor; keeps its int32 arrays alive."""
 
-    def __init__(self, q_lens=None, cache_lens=None, frame_pos0=None, ctx_lens=None):
+    def __init__(self, q_lens=None, cache_lens=None, frame_pos0=None, ctx_lens=None,
+                 sparsity=None):
         lens = [a for a in (q_lens, cache_lens, frame_pos0, ctx_lens) if a is not None]
         n = len(lens[0]) if lens else 0
         self._arrs = []
@@ -178,8 +181,16 @@ class Batch:
             self._arrs.append(c)
             return C.cast(c, C.POINTER(C.c_int32))
 
-        self.struct = ardit_batch(n, arr(q_lens), arr(cache_lens), arr(frame_pos0), arr(ctx_lens))
+        sp = None
+        if sparsity is not None:
+            assert len(sparsity) == n, "all per-stream arrays must have the same length"
+            c = (C.c_float * n)(*[float(v) for v in sparsity])
+            self._arrs.append(c)
+            sp = C.cast(c, C.POINTER(C.c_float))
+        self.struct = ardit_batch(n, arr(q_lens), arr(cache_lens), arr(frame_pos0), arr(ctx_lens),
+                                  sp)
         self.n = n
+        self.q_lens = None if q_lens is None else [int(v) for v in q_lens]
 
 
 def kv_paged(k_pages, v_pages, page_table, n_pages: int, max_frames: int) -> ardit_kv_paged:
@@ -225,6 +236,13 @@ def ardit_kv_append(stream, dims, batch: Batch, qkv, g_q, g_k, kv: ardit_kv_page
 def ardit_attn_fwd(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o, ws, ws_bytes):
     _check(_lib.ardit_attn_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(q),
                                C.byref(kv), _ptr(o), _ptr(ws), int(ws_bytes)), "ardit_attn_fwd")
+
+
+def ardit_sparse_select(stream, dims, batch: Batch, q, kv: ardit_kv_paged, blocks, row_stride,
+                        ws, ws_bytes):
+    _check(_lib.ardit_sparse_select(_stream(stream), C.byref(dims), C.byref(batch.struct),
+                                    _ptr(q), C.byref(kv), _ptr(blocks), int(row_stride), _ptr(ws),
+                                    int(ws_bytes)), "ardit_sparse_select")
 
 
 def ardit_block_fwd(stream, dims, x, kv: ardit_kv_paged, cache_len, frame_pos0, mod, ctx_k,

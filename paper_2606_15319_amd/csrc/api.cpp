@@ -114,6 +114,55 @@ int check_batch(const ardit_dims* d, const ardit_batch* b, unsigned use) {
   }
   if (nq > (1 << 22) || nc > (1 << 22))
     return fail(ARDIT_ECAPACITY, "more than 2^22 tokens in one batch");
+  if (b->sparsity)
+    for (int i = 0; i < b->n_streams; ++i) {
+      const float r = b->sparsity[i];
+      if (!(r >= 0.f && r <= 1.f))
+        return fail(ARDIT_EINVAL, "sparsity[%d] = %g not in [0, 1]", i, static_cast<double>(r));
+    }
+  return ARDIT_OK;
+}
+
+// true when some stream of the batch runs block-sparse self-attention
+bool batch_sparse(const ardit_batch* b) {
+  if (!b->sparsity) return false;
+  for (int i = 0; i < b->n_streams; ++i)
+    if (b->sparsity[i] > 0.f) return true;
+  return false;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Bytes of the block selection's scratch for this batch: fp32 key-tile means
+// and the kept-tile lists, packed per stream.
+void sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b, size_t* kbar, size_t* lists) {
+  *kbar = *lists = 0;
+  if (!batch_sparse(b) || !b->q_lens || !b->cache_lens) return;
+  for (int i = 0; i < b->n_streams; ++i) {
+    const int64_t q = b->q_lens[i];
+    if (q <= 0) continue;
+    const int64_t nt = ceil_div(b->cache_lens[i] + q, kAttnKTile);
+    const int64_t nk = sparse_keep_count(static_cast<int>(nt), b->sparsity[i]);
+    *kbar += sizeof(float) * static_cast<size_t>(d->n_heads * nt * d->head_dim);
+    *lists += sizeof(int32_t) * static_cast<size_t>(d->n_heads * ceil_div(q, kAttnQTile) * nk);
+  }
+}
+
+// Limits of the block selection, on a batch whose q_lens and cache_lens passed check_batch.
+int check_sparse(const ardit_dims* d, const ardit_batch* b) {
+  if (!b->sparsity) return ARDIT_OK;
+  int64_t lists = 0;
+  for (int i = 0; i < b->n_streams; ++i) {
+    const int64_t q = b->q_lens[i];
+    if (q <= 0) continue;
+    const int64_t nt = ceil_div(b->cache_lens[i] + q, kAttnKTile);
+    if (b->sparsity[i] > 0.f && nt > kSparseMaxTiles)
+      return fail(ARDIT_EUNSUPPORTED, "stream %d: %lld key tiles above the %d the selection ranks",
+                  i, static_cast<long long>(nt), kSparseMaxTiles);
+    lists += d->n_heads * ceil_div(q, kAttnQTile) *
+             sparse_keep_count(static_cast<int>(nt), b->sparsity[i]);
+  }
+  if (lists >= (int64_t(1) << 31)) return fail(ARDIT_ECAPACITY, "kept-tile lists above 2^31 entries");
   return ARDIT_OK;
 }
 
@@ -172,10 +221,12 @@ struct Ws {
   size_t h, qkv, q, o, x1, x2, u;    // bf16 block activations
   size_t ck, cv;                     // bf16 text projections
   size_t attn;                       // fp32 partial results of split attention
+  size_t sp_kbar, sp_lists;          // block-sparse selection (last, sized by the batch)
   size_t total;
 };
 
-Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc) {
+Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc, size_t kbar_bytes = 0,
+             size_t list_bytes = 0) {
   Ws w;
   size_t off = 0;
   const size_t D = d->dim, F = d->ffn_dim;
@@ -197,6 +248,8 @@ Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc) {
   w.ck = take(2 * Nc * D);
   w.cv = take(2 * Nc * D);
   w.attn = take(attention_split_bytes(d->head_dim));
+  w.sp_kbar = take(kbar_bytes);
+  w.sp_lists = take(list_bytes);
   w.total = off;
   return w;
 }
@@ -216,7 +269,9 @@ int64_t sum_ctx(const ardit_batch* b) {
 
 int check_ws(const ardit_dims* d, const ardit_batch* b, const void* ws, size_t ws_bytes,
              Ws* out) {
-  *out = ws_layout(d, b->n_streams, sum_q(b), sum_ctx(b));
+  size_t kb = 0, lb = 0;
+  sparse_ws_bytes(d, b, &kb, &lb);
+  *out = ws_layout(d, b->n_streams, sum_q(b), sum_ctx(b), kb, lb);
   if (!ws) return fail(ARDIT_EINVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
     return fail(ARDIT_EINVAL, "workspace must be %zu-byte aligned", kAlign);
@@ -281,7 +336,8 @@ hipEvent_t take_event(Timing& t) {
   return e;
 }
 
-// launches the self-attention kernel, bracketed by events while timing is on
+// launches the self-attention kernels (block selection first when sparse),
+// bracketed by events while timing is on
 int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
   Timing& tm = timing();
   hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -293,7 +349,12 @@ int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
     }
   }
   if (e0 && e1) ARDIT_HIP(hipEventRecord(e0, st), "hipEventRecord");
-  ARDIT_HIP(launch_attention(st, a, hd, true), "self-attention launch");
+  if (a.blocks) {
+    ARDIT_HIP(launch_sparse_select(st, a, hd), "block selection launch");
+    ARDIT_HIP(launch_sparse_attention(st, a, hd), "block-sparse attention launch");
+  } else {
+    ARDIT_HIP(launch_attention(st, a, hd, true), "self-attention launch");
+  }
   if (e0 && e1) {
     ARDIT_HIP(hipEventRecord(e1, st), "hipEventRecord");
     std::lock_guard<std::mutex> g(tm.mu);
@@ -302,8 +363,9 @@ int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
   return ARDIT_OK;
 }
 
-AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
-                        const ardit_kv_paged* kv, void* o, float* split_ws) {
+// Self-attention over the pages, streams in batch order, not yet planned.
+AttnArgs self_attn_base(const ardit_dims* d, const ardit_batch* b, const void* q,
+                        const ardit_kv_paged* kv, void* o) {
   AttnArgs a;
   memset(&a, 0, sizeof(a));
   a.q = static_cast<const bf16_t*>(q);
@@ -331,7 +393,18 @@ AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q
     s.T = a.T;
     row += b->q_lens[i];
   }
-  plan_attention(a, d->head_dim, split_ws);
+  return a;
+}
+
+// Planned self-attention.  Sparse batches run the block-sparse kernels with
+// their lists and key means in the workspace regions of L.
+AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
+                        const ardit_kv_paged* kv, void* o, void* ws, const Ws& L) {
+  AttnArgs a = self_attn_base(d, b, q, kv, o);
+  if (batch_sparse(b))
+    plan_sparse_attention(a, b->sparsity, at<int32_t>(ws, L.sp_lists), 0, at<float>(ws, L.sp_kbar));
+  else
+    plan_attention(a, d->head_dim, at<float>(ws, L.attn));
   return a;
 }
 
@@ -403,7 +476,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
                                kv->page_table, kv->max_frames, kv->n_pages, rs),
             "v_append");
   // self-attention over [cache | chunk]
-  const AttnArgs sa = self_attn_args(d, b, q, kv, o, at<float>(ws, L.attn));
+  const AttnArgs sa = self_attn_args(d, b, q, kv, o, ws, L);
   ARDIT_TRY(run_self_attention(st, sa, hd));
   // x1 = x + gate1 * (o W_o^T + b_o)
   e = GemmEpiArgs();
@@ -458,6 +531,7 @@ int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
   ARDIT_TRY(check_dims(d));
   ARDIT_TRY(check_batch(d, b, kUseQ | kUseCache | kUsePos | kUseCtx | kChunkQ));
   ARDIT_TRY(check_kv(d, b, kv));
+  ARDIT_TRY(check_sparse(d, b));
   ARDIT_TRY(check_ptr(x, "x"));
   ARDIT_TRY(check_ptr(out, "out"));
   ARDIT_TRY(check_ptr(mod, "mod"));
@@ -487,7 +561,7 @@ const char* ardit_status_str(int s) {
 
 const char* ardit_last_error(void) { return g_last_error.c_str(); }
 
-int ardit_version(void) { return 200; }
+int ardit_version(void) { return 300; }
 
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) {
   ARDIT_TRY(check_dims(dims));
@@ -495,7 +569,15 @@ int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_
   ARDIT_TRY(check_batch(dims, batch, 0));
   if (batch->q_lens) ARDIT_TRY(check_batch(dims, batch, kUseQ));
   if (batch->ctx_lens) ARDIT_TRY(check_batch(dims, batch, kUseCtx));
-  *bytes = ws_layout(dims, batch->n_streams, sum_q(batch), sum_ctx(batch)).total;
+  if (batch_sparse(batch)) {
+    if (!batch->q_lens || !batch->cache_lens)
+      return fail(ARDIT_EINVAL, "a sparse batch needs q_lens and cache_lens");
+    ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
+    ARDIT_TRY(check_sparse(dims, batch));
+  }
+  size_t kb = 0, lb = 0;
+  sparse_ws_bytes(dims, batch, &kb, &lb);
+  *bytes = ws_layout(dims, batch->n_streams, sum_q(batch), sum_ctx(batch), kb, lb).total;
   return ARDIT_OK;
 }
 
@@ -595,12 +677,47 @@ int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
   ARDIT_TRY(check_kv(dims, batch, kv));
+  ARDIT_TRY(check_sparse(dims, batch));
   ARDIT_TRY(check_ptr(q, "q"));
   ARDIT_TRY(check_ptr(o, "o"));
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
-  const AttnArgs a = self_attn_args(dims, batch, q, kv, o, at<float>(ws, L.attn));
+  const AttnArgs a = self_attn_args(dims, batch, q, kv, o, ws, L);
   return run_self_attention(stream, a, dims->head_dim);
+}
+
+int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                        const void* q, const ardit_kv_paged* kv, int32_t* blocks,
+                        int32_t row_stride, void* ws, size_t ws_bytes) {
+  ARDIT_TRY(check_dims(dims));
+  ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
+  ARDIT_TRY(check_kv(dims, batch, kv));
+  ARDIT_TRY(check_sparse(dims, batch));
+  ARDIT_TRY(check_ptr(q, "q"));
+  if (!blocks) return fail(ARDIT_EINVAL, "blocks is NULL");
+  if (reinterpret_cast<uintptr_t>(blocks) % sizeof(int32_t) != 0)
+    return fail(ARDIT_EINVAL, "blocks must be 4-byte aligned");
+  int64_t rows = 0;
+  int max_keep = 0;
+  for (int i = 0; i < batch->n_streams; ++i) {
+    const int64_t qn = batch->q_lens[i];
+    if (qn <= 0) continue;
+    const int nt = static_cast<int>(ceil_div(batch->cache_lens[i] + qn, kAttnKTile));
+    const int nk = sparse_keep_count(nt, batch->sparsity ? batch->sparsity[i] : 0.f);
+    max_keep = nk > max_keep ? nk : max_keep;
+    rows += dims->n_heads * ceil_div(qn, kAttnQTile);
+  }
+  if (row_stride < max_keep)
+    return fail(ARDIT_EINVAL, "row_stride %d below the %d tiles a row keeps", row_stride,
+                max_keep);
+  if (rows * row_stride >= (int64_t(1) << 31))
+    return fail(ARDIT_ECAPACITY, "block lists above 2^31 entries");
+  Ws L;
+  ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  AttnArgs a = self_attn_base(dims, batch, q, kv, nullptr);
+  plan_sparse_attention(a, batch->sparsity, blocks, row_stride, at<float>(ws, L.sp_kbar));
+  ARDIT_HIP(launch_sparse_select(stream, a, dims->head_dim), "block selection launch");
+  return ARDIT_OK;
 }
 
 int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
@@ -625,6 +742,7 @@ int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x, a
   b.cache_lens = &cache_len;
   b.frame_pos0 = &frame_pos0;
   b.ctx_lens = &ctx_len;
+  b.sparsity = nullptr;
   return ardit_block_fwd_varlen(stream, dims, &b, x, &kv, mod, ctx_k, ctx_v, w, out, ws,
                                 ws_bytes);
 }

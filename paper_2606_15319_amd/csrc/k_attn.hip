@@ -210,11 +210,13 @@ __device__ __forceinline__ void store_partial(const AttnArgs& a, size_t slot,
 
 // Runs key tiles [tb, te) of item (S, head h, query tile qt) over the
 // workgroup's 256 queries, then writes the normalised output (slot < 0) or
-// the partial results into slot `slot`.
-template <int HD, bool PAGED, bool VEC>
+// the partial results into slot `slot`.  LIST: positions [tb, te) index the
+// tile list tl (block-sparse attention) instead of being the tiles themselves.
+template <int HD, bool PAGED, bool VEC, bool LIST = false>
 __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& S, int h, int qt,
                                            int tb, int te, bf16_t (&sK)[2][BKV * HD],
-                                           bf16_t (&sV)[2][HD * BKV], int64_t slot) {
+                                           bf16_t (&sV)[2][HD * BKV], int64_t slot,
+                                           const int32_t* tl = nullptr) {
   constexpr int KLD = HD;              // LDS row of the key tile
   constexpr int VLD = BKV;             // LDS row of the value tile
   constexpr int NK = BKV * HD / 8 / NTHR;   // 16-byte key chunks per thread per tile
@@ -308,9 +310,12 @@ __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& 
       *reinterpret_cast<u32x4*>(&sV[buf][v_lds[i]]) = rv[set][i];                        \
 }
 
+  // list entries are clamped into the stream's tiles, so a corrupt list cannot
+  // send the loads outside the pages
+#define ARDIT_TIX(t) (LIST ? min(max(tl[(t)], 0), S.n_tiles - 1) : (t))
   // two tiles of loads in flight: register set (t - tb) & 1 holds tile t until stored
-  ARDIT_LOAD(tb, 0);
-  if (tb + 1 < te) ARDIT_LOAD(tb + 1, 1);
+  ARDIT_LOAD(ARDIT_TIX(tb), 0);
+  if (tb + 1 < te) ARDIT_LOAD(ARDIT_TIX(tb + 1), 1);
   ARDIT_STORE(0, 0);
   __syncthreads();
   for (int t0 = tb; t0 < te; t0 += 2) {
@@ -319,7 +324,7 @@ __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& 
       const int t = t0 + half;
       if (t < te) {
         const int buf = half;
-        if (t + 2 < te) ARDIT_LOAD(t + 2, half);
+        if (t + 2 < te) ARDIT_LOAD(ARDIT_TIX(t + 2), half);
         // S^T = K Q^T: four 16-key blocks x two 16-query blocks, 8 accumulators
         f32x4 s[4][2];
 #pragma unroll
@@ -352,12 +357,13 @@ __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& 
           }
           __builtin_amdgcn_sched_group_barrier(0x008, 2 * LDS_AHEAD, 0);
         }
-        if (t >= nfull) {   // keys past the end (last tile only)
+        const int tile = ARDIT_TIX(t);
+        if (tile >= nfull) {   // keys past the end (last tile only)
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-              const int key = t * BKV + kappa16(kb, 4 * g + v);
+              const int key = tile * BKV + kappa16(kb, 4 * g + v);
               if (key >= kv_len) {
                 s[kb][0][v] = -INFINITY;
                 s[kb][1][v] = -INFINITY;
@@ -435,6 +441,7 @@ __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& 
   }
 #undef ARDIT_LOAD
 #undef ARDIT_STORE
+#undef ARDIT_TIX
   if (slot < 0)
     store_output<HD>(a, S, h, qt, o, l_run);
   else
@@ -799,7 +806,40 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const AttnArgs a) {
   }
 }
 
+// Block-sparse attention: one workgroup per item over the item's kept tiles,
+// read from its list (written by the block selection).
+template <int HD>
+__global__ __launch_bounds__(NTHR, 1) void attn_sparse_kernel(const AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * HD];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * BKV];
+  const int pid = blockIdx.x;
+  const int L = (pid % kNumXcd) * a.per_xcd + pid / kNumXcd;
+  if (L >= a.total_items) return;
+  int si = 0;
+  for (int i = 1; i < a.n_streams; ++i)
+    if (L >= a.s[i].item_begin) si = i;
+  const AttnStream S = a.s[si];
+  const int it = L - S.item_begin;
+  const int h = it / S.n_qtiles;
+  const int qt = it - h * S.n_qtiles;
+  const int ld = a.blk_ld ? a.blk_ld : S.n_keep;
+  const int32_t* tl = a.blocks + S.blk_off + static_cast<int64_t>(it) * ld;
+  attn_range<HD, true, true, true>(a, S, h, qt, 0, S.n_keep, sK, sV, -1, tl);
+}
+
 }  // namespace
+
+hipError_t launch_sparse_attention(hipStream_t st, const AttnArgs& a, int head_dim) {
+  if (a.total_items == 0) return hipSuccess;
+  const dim3 grid(a.per_xcd * kNumXcd);
+  if (head_dim == 128)
+    hipLaunchKernelGGL((attn_sparse_kernel<128>), grid, dim3(NTHR), 0, st, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL((attn_sparse_kernel<64>), grid, dim3(NTHR), 0, st, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 size_t attention_split_bytes(int head_dim) {
   return static_cast<size_t>(2) * kAttnSplitBlocks * BQ * (head_dim + 2) * sizeof(float);

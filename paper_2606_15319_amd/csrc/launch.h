@@ -11,6 +11,12 @@ namespace ardit {
 constexpr int kMaxStreams = 64;
 // workgroups of a split attention schedule (one per CU of an MI355X)
 constexpr int kAttnSplitBlocks = 256;
+// attention work-item shape: 256 queries by 64-key tiles; block-sparse
+// attention selects whole tiles per (stream, head, query tile)
+constexpr int kAttnQTile = 256;
+constexpr int kAttnKTile = 64;
+// key tiles of one stream that the block selection can rank (64 KB of LDS)
+constexpr int kSparseMaxTiles = 16384;
 
 // ---------------------------------------------------------------- GEMM
 enum GemmEpi : int {
@@ -51,6 +57,8 @@ struct AttnStream {
   int32_t n_tiles;     // 64-key tiles of kv_len
   int32_t main_tiles;  // split schedule: tiles [0, main_tiles) run in the item's own workgroup
   int32_t tail_begin;  // split schedule: first tail tile of the stream's items, concatenated
+  int32_t n_keep;      // block-sparse: key tiles kept per item (n_tiles when dense)
+  int32_t blk_off;     // block-sparse: element offset of the stream's kept-tile lists
 };
 
 struct AttnArgs {
@@ -75,8 +83,13 @@ struct AttnArgs {
   int32_t split_tiles;   // split: tail tiles per spare workgroup
   float* part_o;         // [2 split_blocks][256][d] partial unnormalised outputs
   float* part_ml;        // [2 split_blocks][2][256] partial running max, denominator
+  int32_t* blocks;       // block-sparse: kept tiles of item (h, qt) of stream S at
+                         // blocks + S.blk_off + (h n_qtiles + qt) * ld, ascending
+  int32_t blk_ld;        // row stride of those lists; 0: the stream's n_keep
+  float* kbar;           // block-sparse: fp32 mean key of every (stream, head, tile)
   AttnStream s[kMaxStreams];
 };
+static_assert(sizeof(AttnArgs) <= 4096, "attention arguments must fit the kernel-argument buffer");
 
 // Device bytes of the partial results of a split schedule.
 size_t attention_split_bytes(int head_dim);
@@ -85,6 +98,23 @@ size_t attention_split_bytes(int head_dim);
 // split) receives the partial results when the items are cut between workgroups.
 void plan_attention(AttnArgs& a, int head_dim, float* split_ws);
 hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, bool paged);
+
+// ------------------------------------------------- block-sparse attention
+// Key tiles kept per query tile at sparsity rho: ceil((1 - rho) n - 1e-3) in [1, n].
+int sparse_keep_count(int n_tiles, float rho);
+// fp32 floats of the key-tile means of these streams (kbar).
+size_t sparse_kbar_floats(const AttnArgs& a, int head_dim);
+// Plans a block-sparse self-attention over paged keys: n_keep per stream from
+// rho (batch order, before planning), one workgroup per item, streams ordered
+// by decreasing n_keep.  blocks / blk_ld: where the selection writes its lists
+// (blk_ld 0: packed per stream); kbar: sparse_kbar_floats of scratch.
+void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32_t blk_ld,
+                           float* kbar);
+// Selection: key-tile means, then per item the scores mean(q) . mean(k) and
+// its n_keep best tiles, written ascending (padded with -1 up to blk_ld).
+hipError_t launch_sparse_select(hipStream_t st, const AttnArgs& a, int head_dim);
+// Attention of every item over its kept tiles only.
+hipError_t launch_sparse_attention(hipStream_t st, const AttnArgs& a, int head_dim);
 
 // --------------------------------------------------------- elementwise
 struct RowStream {

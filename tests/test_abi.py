@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     for code, name in A.STATUS.items():
         assert A.ardit_status_str(code) == name
     assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
-    assert A.ardit_version() == 200
+    assert A.ardit_version() == 300
 
 
 def _dims(**kw):
@@ -176,3 +176,47 @@ def test_layout_round_trip():
     kf, vf = ctx_to_device_layout(kc, vc, H)
     kc2, vc2 = ctx_from_device_layout(kf, vf, 7, H, d)
     assert np.array_equal(kc, kc2) and np.array_equal(vc, vc2)
+
+
+def test_sparsity_validation():
+    d = _dims()
+    for bad in (1.5, -0.1, float("nan")):
+        assert _status(A.ardit_workspace_size, d, A.Batch([100], [64], sparsity=[bad])) == -1
+        assert "sparsity" in A.ardit_last_error()
+    # more key tiles than the selection ranks (16384 tiles of 64 keys)
+    big = A.Batch([192], [64 * 16384], sparsity=[0.5])
+    assert _status(A.ardit_workspace_size, d, big) == -5
+    # the same length is fine when dense
+    assert A.ardit_workspace_size(d, A.Batch([192], [64 * 16384], sparsity=[0.0])) > 0
+
+
+def test_sparse_workspace_holds_means_and_lists():
+    """Extra workspace of a sparse batch: fp32 key-tile means (H x tiles x d)
+    plus the kept-tile lists (H x query tiles x n_keep int32), each rounded up
+    to 256 bytes; n_keep from the oracle's rule."""
+    from oracle.sparse_ref import keep_count
+    d = _dims()
+    q, c = 768, 6336                       # 3 query tiles; 7104 keys = 111 tiles
+    dense = A.ardit_workspace_size(d, A.Batch([q], [c]))
+    assert A.ardit_workspace_size(d, A.Batch([q], [c], sparsity=[0.0])) == dense
+    up = lambda n: (n + 255) // 256 * 256
+    for rho in (0.6, 0.7, 0.8, 0.9, 1.0):
+        nk = keep_count(111, rho)
+        want = dense + up(4 * 111 * 64 * 4) + up(4 * 3 * nk * 4)
+        assert A.ardit_workspace_size(d, A.Batch([q], [c], sparsity=[rho])) == want, rho
+
+
+def test_sparse_select_validation():
+    d = _dims()
+    b = A.Batch([600, 70], [1280, 192], sparsity=[0.8, 1.0])
+    need = A.ardit_workspace_size(d, b)
+    # stream 0 keeps ceil(0.2 * 30) = 6 of its 30 tiles
+    assert _status(A.ardit_sparse_select, FAKE, d, b, FAKE, _kv(max_frames=40), FAKE, 5, FAKE,
+                   need) == -1
+    assert "row_stride" in A.ardit_last_error()
+    assert _status(A.ardit_sparse_select, FAKE, d, b, FAKE, _kv(max_frames=40), 0, 6, FAKE,
+                   need) == -1
+    assert _status(A.ardit_sparse_select, FAKE, d, b, FAKE, _kv(max_frames=40), FAKE, 6, FAKE,
+                   need - 1) == -4
+    assert _status(A.ardit_sparse_select, FAKE, d, b, FAKE, _kv(max_frames=4), FAKE, 6, FAKE,
+                   need) == -3

@@ -438,3 +438,150 @@ def test_block_full_size_sampled_rows(A, name):
                                              int(np.argmax(run.case.cache_len))})
     for b in streams:
         _check_block(run, b, rows=sample_rows(sh.chunk_tokens, seed=b), tag=name)
+
+
+# ----------------------------------------------------- block-sparse attention
+S = O.sparse_ref
+
+
+def _sparse_rows(A, dims, batch, q, kv, row_stride):
+    """ardit_sparse_select into a fresh [rows][row_stride] int32 buffer."""
+    import torch
+    n = A.ardit_workspace_size(dims, batch)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    H = dims.n_heads
+    rows = H * sum((n + 255) // 256 for n in batch.q_lens)
+    blocks = torch.full((rows, row_stride), -7, dtype=torch.int32, device="cuda")
+    A.ardit_sparse_select(None, dims, batch, q, kv, blocks, row_stride, ws, n)
+    _sync()
+    return blocks.cpu().numpy()
+
+
+def _check_selection(got, qs, ks, rho, H, tag, rel_tol=1e-5):
+    """got: [H * n_qtiles, stride] rows of one stream.  Equal to the oracle's
+    fp32 selection, except that a tile may trade places with one whose float64
+    score is within rel_tol of it (rounding order); -1 padding after n_keep.
+    Returns the lists [H, n_qtiles, n_keep]."""
+    n_k = (ks.shape[0] + S.K_BLOCK - 1) // S.K_BLOCK
+    nk = S.keep_count(n_k, rho)
+    nq = (qs.shape[0] + S.Q_BLOCK - 1) // S.Q_BLOCK
+    got = got.reshape(H, nq, -1)
+    assert (got[:, :, nk:] == -1).all(), f"{tag}: padding"
+    lists = got[:, :, :nk]
+    ref = S.select_blocks(S.block_scores(qs, ks), nk)
+    s64 = S.block_scores(qs, ks, dtype=np.float64)
+    n_diff = 0
+    for h in range(H):
+        for i in range(nq):
+            g = lists[h, i]
+            assert (np.diff(g) > 0).all() and g[0] >= 0 and g[-1] < n_k, f"{tag}: list {g}"
+            if not np.array_equal(g, ref[h, i]):
+                n_diff += 1
+                sc = s64[h, i]
+                tol = rel_tol * np.abs(sc).max()
+                dropped = np.setdiff1d(np.arange(n_k), g)
+                assert sc[g].min() >= sc[dropped].max() - tol, f"{tag}: wrong tiles h={h} i={i}"
+    assert n_diff <= max(1, H * nq // 50), f"{tag}: {n_diff} rows differ from the oracle"
+    return lists
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_sparse_select_and_attention_ragged(A, hd):
+    """Four streams with rho 0.8, 0 (every tile), 0.6 and 1 (one tile), ragged
+    query and key tiles, pages shuffled: the lists match the oracle's selection
+    (ascending, -1 padded to the row stride) and the attention over them
+    matches the oracle's masked attention on every row."""
+    sh = BlockShape(dim=4 * hd, n_heads=4, head_dim=hd, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    q_lens, caches, rho = [600, 256, 300, 70], [1280, 0, 640, 192], [0.8, 0.0, 0.6, 1.0]
+    pc, dims, _, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 60)
+    batch = A.Batch(q_lens, caches, sparsity=rho)
+    H = sh.n_heads
+    rows = _sparse_rows(A, dims, batch, q, pc.kv(A), row_stride=9)
+    _attn(A, dims, batch, q, pc.kv(A), o)
+    _sync()
+    og = host_f32(o)
+    off = r0 = 0
+    for b, n in enumerate(q_lens):
+        nq = (n + 255) // 256
+        lists = _check_selection(rows[r0:r0 + H * nq], qs[b], ks[b], rho[b], H, f"stream {b}")
+        if rho[b] == 0.0:
+            assert (lists == np.arange(lists.shape[-1])).all()
+        ref = S.sparse_attention(qs[b], ks[b], vs[b], lists).reshape(n, -1)
+        parity(og[off:off + n], ref, f"sparse attn hd={hd} stream {b}", quantum=ref)
+        off += n
+        r0 += H * nq
+
+
+@pytest.mark.parametrize("rho", [0.6, 0.9])
+def test_sparse_attention_4680x14040(A, rho):
+    """4680 queries over 14040 keys, 12 heads of 128, QK-RMSNorm applied: every
+    item's list against the oracle's selection, sampled rows of the attention."""
+    import torch
+    wl = WORKLOADS["attn"]
+    sh = wl.shape
+    rng = make_rng(wl.wid)
+    L, c = sh.chunk_tokens, 2 * sh.chunk_tokens
+    H, d, D = sh.n_heads, sh.head_dim, sh.dim
+    q = bf16_round(O.rms_norm(rng.standard_normal((L, D), dtype=np.float32), sh.eps))
+    k = bf16_round(O.rms_norm(rng.standard_normal((c + L, D), dtype=np.float32), sh.eps))
+    v = normal_bf16(rng, (c + L, H, d))
+    T = sh.tokens_per_frame
+    pc = PagedCache(sh, [list(range((c + L) // T))], (c + L) // T)
+    pc.fill_stream(0, k.reshape(-1, H, d), v)
+    pc.upload()
+    qd = dev_bf16(q)
+    o = torch.empty_like(qd)
+    dims = A.dims_from_shape(sh)
+    batch = A.Batch([L], [c], sparsity=[rho])
+    nk = S.keep_count((c + L + 63) // 64, rho)
+    rows = _sparse_rows(A, dims, batch, qd, pc.kv(A), row_stride=nk)
+    lists = _check_selection(rows, q.reshape(L, H, d), k.reshape(-1, H, d), rho, H, f"rho={rho}")
+    _attn(A, dims, batch, qd, pc.kv(A), o)
+    _sync()
+    sel = sample_rows(L, seed=3)
+    ref = S.sparse_attention(q.reshape(L, H, d), k.reshape(-1, H, d), v, lists,
+                             rows=sel).reshape(len(sel), D)
+    parity(host_f32(o)[sel], ref, f"sparse attn 4680x14040 rho={rho}", quantum=ref)
+
+
+def test_sparse_block_varlen(A):
+    """A ragged batch of four tiny-shape streams at rho 0.6 / 0.9 / 0.7 / 0.8
+    through the block call.  The oracle selects from its bf16-rounded q and k;
+    the kernels score their own bf16 values, so a stream is compared only when
+    no item of it has two tiles at its keep boundary closer than 1% of the
+    row's largest score (at least two of the four must qualify)."""
+    from workloads.gen import Workload
+    wl = Workload(11, "sparse_tiny", WORKLOADS["tiny"].shape, cache_chunks=(2, 4, 0, 6),
+                  frame_pos0=(6, 12, 0, 18), ctx_len=32, timesteps=(750, 500, 1000, 250))
+    rho = [0.6, 0.9, 0.7, 0.8]
+    run = BlockRun(wl, A)
+    c = run.case
+    import torch
+    run.batch = A.Batch([run.shape.chunk_tokens] * 4, c.cache_len, c.frame_pos0,
+                        [a.shape[0] for a in c.ctx], sparsity=rho)
+    run.ws_bytes = A.ardit_workspace_size(run.dims, run.batch)
+    run.ws = torch.empty(run.ws_bytes, dtype=torch.uint8, device="cuda")
+    run.run()
+    _sync()
+    sh = run.shape
+    L = sh.chunk_tokens
+    out = host_f32(run.out)
+    checked = 0
+    for b in range(4):
+        m_t = O.time_modulation(c.t[b], c.time_w, sh.dim)
+        kc, vc = O.context_kv(c.ctx[b], c.block_w, sh.eps)
+        ref = O.block_forward(c.x[b], c.cache_k[b], c.cache_v[b], c.frame_pos0[b], m_t, kc, vc,
+                              c.block_w, sh, rho=rho[b])
+        K = np.concatenate([c.cache_k[b], ref["k_new"]])
+        sc = S.block_scores(bf16_round(ref["q"]), bf16_round(K), dtype=np.float64)
+        nk = ref["blocks"].shape[-1]
+        srt = -np.sort(-sc, axis=-1)
+        if nk < sc.shape[-1]:
+            margin = srt[..., nk - 1] - srt[..., nk]
+            if (margin < 1e-2 * np.abs(sc).max(axis=-1)).any():
+                continue
+        checked += 1
+        parity(out[b * L:(b + 1) * L], ref["out"], f"sparse block out stream {b}")
+        parity(out[b * L:(b + 1) * L] - c.x[b], ref["out"] - c.x[b], f"sparse out-x stream {b}",
+               tol=5e-2, quantum=ref["out"], cos_ref=bf16_round(ref["out"]) - c.x[b])
+    assert checked >= 2, f"only {checked} streams had an unambiguous selection"
