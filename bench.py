@@ -15,11 +15,18 @@ one block step of layer 0 (cpu_baseline).  roofline.traffic is the HBM bytes
 per attention launch measured with rocprofv3 counters (FETCH_SIZE and
 WRITE_SIZE, FETCH_SIZE scaled by what it reads for a plain copy of known
 size, see --copy-probe), taken from the profile summary under profiles/ when
-that summary was made from the current attention sources, else null."""
+that summary was made from the current attention sources, else null.
+
+--sparsity RHO runs the same workload with block-sparse self-attention at
+sparsity RHO (the fidelity knob; every 256-query tile keeps
+ceil((1 - RHO) 512) of the 512 key tiles of 64): the step then also runs the
+block selection, and the roofline counts the attention kernel's kept keys,
+4 L_q (n_keep 64) D flops per launch."""
 from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -43,6 +50,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--layers", type=int, default=LAYERS)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--sparsity", type=float, default=0.0, metavar="RHO",
+                   help="attention sparsity rho of the stream (0: dense)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB on the device 5 times with one kernel (counter calibration)")
     return p.parse_args()
@@ -94,7 +103,7 @@ def copy_probe(mib):
 class Model:
     """Weights, pages and text K/V of every layer, drawn on the device."""
 
-    def __init__(self, A, sh, n_layers, cache_len, ctx_len, dev):
+    def __init__(self, A, sh, n_layers, cache_len, ctx_len, dev, rho=0.0):
         import torch
         self.A, self.sh, self.n_layers = A, sh, n_layers
         D, F, H, d = sh.dim, sh.ffn_dim, sh.n_heads, sh.head_dim
@@ -102,7 +111,9 @@ class Model:
         self.cache_len, self.ctx_len = cache_len, ctx_len
         self.frames = cache_len // T + sh.frames
         self.dims = A.dims_from_shape(sh)
-        self.batch = A.Batch([sh.chunk_tokens], [cache_len], [cache_len // T], [ctx_len])
+        self.rho = rho
+        self.batch = A.Batch([sh.chunk_tokens], [cache_len], [cache_len // T], [ctx_len],
+                             sparsity=[rho])
         self.ws_bytes = A.ardit_workspace_size(self.dims, self.batch)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
         from workloads.gen import block_weight_shapes, GAIN_NAMES
@@ -184,12 +195,13 @@ def cpu_baseline(model):
     m_t = O.time_modulation(TIMESTEPS[0], tw, sh.dim)
     kc, vc = O.context_kv(ctxh, w, sh.eps)
     t_ctx = time.perf_counter()
-    O.block_forward(x, ck, cv, model.cache_len // T, m_t, kc, vc, w, sh)
+    O.block_forward(x, ck, cv, model.cache_len // T, m_t, kc, vc, w, sh, rho=model.rho)
     t1 = time.perf_counter()
     return {"value": round((t1 - t_ctx) * 1e3, 1), "unit": "ms per chunk-denoise-step per block",
             "cores": int(threads), "kind": "oracle",
             "sample": ("one full block step (layer 0, t=1000) of the same workload: 4680 queries "
-                       "over 32760 keys, float64 numpy; text K/V and time modulation "
+                       f"over 32760 keys{' at sparsity %g' % model.rho if model.rho else ''}, "
+                       "float64 numpy; text K/V and time modulation "
                        f"({(t_ctx - t0) * 1e3:.0f} ms) excluded as on the GPU path")}
 
 
@@ -212,7 +224,7 @@ def main():
     sh = wl.shape
     cache_len = wl.cache_chunks[0] * sh.chunk_tokens
     log(f"drawing {args.layers} layers on the device")
-    model = Model(A, sh, args.layers, cache_len, wl.ctx_len, dev)
+    model = Model(A, sh, args.layers, cache_len, wl.ctx_len, dev, rho=args.sparsity)
     torch.cuda.synchronize()
     log("warmup")
     for k in range(args.warmup):
@@ -234,7 +246,12 @@ def main():
     ms_step = total_ms / args.steps
     ms_block = ms_step / args.layers
     L_q, L_k, D = sh.chunk_tokens, cache_len + sh.chunk_tokens, sh.dim
-    attn_flops = 4.0 * L_q * L_k * D
+    n_tiles = (L_k + 63) // 64
+    keys = L_k
+    if args.sparsity > 0:
+        n_keep = max(1, min(n_tiles, math.ceil((1.0 - args.sparsity) * n_tiles - 1e-3)))
+        keys = min(L_k, 64 * n_keep)
+    attn_flops = 4.0 * L_q * keys * D
     attn_avg_ms = attn_ms / max(n_attn, 1)
     achieved = attn_flops / (attn_avg_ms * 1e-3) / 1e12
     log(f"{ms_step:.3f} ms/step, {ms_block:.4f} ms/block, attention {attn_avg_ms:.4f} ms "
@@ -261,10 +278,13 @@ def main():
                                "chunk 4680 tokens (3x30x52) over a 28080-token cache, "
                                "512 text tokens, 30 layers, t=1000/750/500/250",
                    "layers": args.layers, "chunk_tokens": L_q, "kv_tokens": L_k,
-                   "ctx_tokens": wl.ctx_len},
+                   "ctx_tokens": wl.ctx_len, "sparsity": args.sparsity,
+                   "attended_keys": keys},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(), "kernel": "paged self-attention",
+                     "traffic": None if args.sparsity else measured_traffic(),
+                     "kernel": ("block-sparse paged self-attention" if args.sparsity
+                                else "paged self-attention"),
                      "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},
         "cpu_baseline": cpu,
     }

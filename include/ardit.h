@@ -234,7 +234,8 @@ int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batc
                     const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes);
 
 /* Kernel timing: while enabled, block calls record HIP events on their stream
- * around every launch of the self-attention kernel.  ardit_timing_collect
+ * around every launch of the self-attention kernel (for sparse streams the
+ * attention over the kept tiles, after the block selection).  ardit_timing_collect
  * waits for the recorded events, returns the number of launches and their
  * summed duration in ms, and clears the record. */
 int ardit_timing_enable(int enable);

@@ -133,25 +133,32 @@ bool batch_sparse(const ardit_batch* b) {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Bytes of the block selection's scratch for this batch: fp32 key-tile means
-// and the kept-tile lists, packed per stream.
-void sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b, size_t* kbar, size_t* lists) {
-  *kbar = *lists = 0;
-  if (!batch_sparse(b) || !b->q_lens || !b->cache_lens) return;
+// Bytes of the block selection's scratch for this batch: the fp32 mean query
+// of every item, its fp32 score per key tile, and the kept-tile lists packed
+// per stream.
+struct SparseBytes {
+  size_t qbar = 0, scores = 0, lists = 0;
+};
+SparseBytes sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b) {
+  SparseBytes z;
+  if (!batch_sparse(b) || !b->q_lens || !b->cache_lens) return z;
   for (int i = 0; i < b->n_streams; ++i) {
     const int64_t q = b->q_lens[i];
     if (q <= 0) continue;
     const int64_t nt = ceil_div(b->cache_lens[i] + q, kAttnKTile);
     const int64_t nk = sparse_keep_count(static_cast<int>(nt), b->sparsity[i]);
-    *kbar += sizeof(float) * static_cast<size_t>(d->n_heads * nt * d->head_dim);
-    *lists += sizeof(int32_t) * static_cast<size_t>(d->n_heads * ceil_div(q, kAttnQTile) * nk);
+    const int64_t items = d->n_heads * ceil_div(q, kAttnQTile);
+    z.qbar += sizeof(float) * static_cast<size_t>(items * d->head_dim);
+    z.scores += sizeof(float) * static_cast<size_t>(items * nt);
+    z.lists += sizeof(int32_t) * static_cast<size_t>(items * nk);
   }
+  return z;
 }
 
 // Limits of the block selection, on a batch whose q_lens and cache_lens passed check_batch.
 int check_sparse(const ardit_dims* d, const ardit_batch* b) {
   if (!b->sparsity) return ARDIT_OK;
-  int64_t lists = 0;
+  int64_t lists = 0, scores = 0;
   for (int i = 0; i < b->n_streams; ++i) {
     const int64_t q = b->q_lens[i];
     if (q <= 0) continue;
@@ -161,8 +168,10 @@ int check_sparse(const ardit_dims* d, const ardit_batch* b) {
                   i, static_cast<long long>(nt), kSparseMaxTiles);
     lists += d->n_heads * ceil_div(q, kAttnQTile) *
              sparse_keep_count(static_cast<int>(nt), b->sparsity[i]);
+    scores += d->n_heads * ceil_div(q, kAttnQTile) * nt;
   }
   if (lists >= (int64_t(1) << 31)) return fail(ARDIT_ECAPACITY, "kept-tile lists above 2^31 entries");
+  if (scores >= (int64_t(1) << 31)) return fail(ARDIT_ECAPACITY, "block scores above 2^31 entries");
   return ARDIT_OK;
 }
 
@@ -221,12 +230,12 @@ struct Ws {
   size_t h, qkv, q, o, x1, x2, u;    // bf16 block activations
   size_t ck, cv;                     // bf16 text projections
   size_t attn;                       // fp32 partial results of split attention
-  size_t sp_kbar, sp_lists;          // block-sparse selection (last, sized by the batch)
+  size_t sp_qbar, sp_scores, sp_lists;   // block-sparse selection (last, sized by the batch)
   size_t total;
 };
 
-Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc, size_t kbar_bytes = 0,
-             size_t list_bytes = 0) {
+Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc,
+             const SparseBytes& sp = SparseBytes()) {
   Ws w;
   size_t off = 0;
   const size_t D = d->dim, F = d->ffn_dim;
@@ -248,8 +257,9 @@ Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc, size_t kbar_byte
   w.ck = take(2 * Nc * D);
   w.cv = take(2 * Nc * D);
   w.attn = take(attention_split_bytes(d->head_dim));
-  w.sp_kbar = take(kbar_bytes);
-  w.sp_lists = take(list_bytes);
+  w.sp_qbar = take(sp.qbar);
+  w.sp_scores = take(sp.scores);
+  w.sp_lists = take(sp.lists);
   w.total = off;
   return w;
 }
@@ -269,9 +279,7 @@ int64_t sum_ctx(const ardit_batch* b) {
 
 int check_ws(const ardit_dims* d, const ardit_batch* b, const void* ws, size_t ws_bytes,
              Ws* out) {
-  size_t kb = 0, lb = 0;
-  sparse_ws_bytes(d, b, &kb, &lb);
-  *out = ws_layout(d, b->n_streams, sum_q(b), sum_ctx(b), kb, lb);
+  *out = ws_layout(d, b->n_streams, sum_q(b), sum_ctx(b), sparse_ws_bytes(d, b));
   if (!ws) return fail(ARDIT_EINVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
     return fail(ARDIT_EINVAL, "workspace must be %zu-byte aligned", kAlign);
@@ -336,8 +344,8 @@ hipEvent_t take_event(Timing& t) {
   return e;
 }
 
-// launches the self-attention kernels (block selection first when sparse),
-// bracketed by events while timing is on
+// launches the self-attention kernels (block selection first when sparse);
+// while timing is on, events bracket the attention kernel itself
 int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
   Timing& tm = timing();
   hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -348,13 +356,12 @@ int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
       e1 = take_event(tm);
     }
   }
+  if (a.blocks) ARDIT_HIP(launch_sparse_select(st, a, hd), "block selection launch");
   if (e0 && e1) ARDIT_HIP(hipEventRecord(e0, st), "hipEventRecord");
-  if (a.blocks) {
-    ARDIT_HIP(launch_sparse_select(st, a, hd), "block selection launch");
+  if (a.blocks)
     ARDIT_HIP(launch_sparse_attention(st, a, hd), "block-sparse attention launch");
-  } else {
+  else
     ARDIT_HIP(launch_attention(st, a, hd, true), "self-attention launch");
-  }
   if (e0 && e1) {
     ARDIT_HIP(hipEventRecord(e1, st), "hipEventRecord");
     std::lock_guard<std::mutex> g(tm.mu);
@@ -402,7 +409,8 @@ AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q
                         const ardit_kv_paged* kv, void* o, void* ws, const Ws& L) {
   AttnArgs a = self_attn_base(d, b, q, kv, o);
   if (batch_sparse(b))
-    plan_sparse_attention(a, b->sparsity, at<int32_t>(ws, L.sp_lists), 0, at<float>(ws, L.sp_kbar));
+    plan_sparse_attention(a, b->sparsity, at<int32_t>(ws, L.sp_lists), 0, at<float>(ws, L.sp_qbar),
+                          at<float>(ws, L.sp_scores));
   else
     plan_attention(a, d->head_dim, at<float>(ws, L.attn));
   return a;
@@ -575,9 +583,8 @@ int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_
     ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
     ARDIT_TRY(check_sparse(dims, batch));
   }
-  size_t kb = 0, lb = 0;
-  sparse_ws_bytes(dims, batch, &kb, &lb);
-  *bytes = ws_layout(dims, batch->n_streams, sum_q(batch), sum_ctx(batch), kb, lb).total;
+  *bytes = ws_layout(dims, batch->n_streams, sum_q(batch), sum_ctx(batch),
+                     sparse_ws_bytes(dims, batch)).total;
   return ARDIT_OK;
 }
 
@@ -715,7 +722,8 @@ int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
   AttnArgs a = self_attn_base(dims, batch, q, kv, nullptr);
-  plan_sparse_attention(a, batch->sparsity, blocks, row_stride, at<float>(ws, L.sp_kbar));
+  plan_sparse_attention(a, batch->sparsity, blocks, row_stride, at<float>(ws, L.sp_qbar),
+                        at<float>(ws, L.sp_scores));
   ARDIT_HIP(launch_sparse_select(stream, a, dims->head_dim), "block selection launch");
   return ARDIT_OK;
 }

@@ -86,7 +86,8 @@ struct AttnArgs {
   int32_t* blocks;       // block-sparse: kept tiles of item (h, qt) of stream S at
                          // blocks + S.blk_off + (h n_qtiles + qt) * ld, ascending
   int32_t blk_ld;        // row stride of those lists; 0: the stream's n_keep
-  float* kbar;           // block-sparse: fp32 mean key of every (stream, head, tile)
+  float* qbar;           // block-sparse: fp32 mean query of every item
+  float* scores;         // block-sparse: fp32 scores, n_tiles per item, streams in plan order
   AttnStream s[kMaxStreams];
 };
 static_assert(sizeof(AttnArgs) <= 4096, "attention arguments must fit the kernel-argument buffer");
@@ -102,16 +103,15 @@ hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, boo
 // ------------------------------------------------- block-sparse attention
 // Key tiles kept per query tile at sparsity rho: ceil((1 - rho) n - 1e-3) in [1, n].
 int sparse_keep_count(int n_tiles, float rho);
-// fp32 floats of the key-tile means of these streams (kbar).
-size_t sparse_kbar_floats(const AttnArgs& a, int head_dim);
 // Plans a block-sparse self-attention over paged keys: n_keep per stream from
 // rho (batch order, before planning), one workgroup per item, streams ordered
 // by decreasing n_keep.  blocks / blk_ld: where the selection writes its lists
-// (blk_ld 0: packed per stream); kbar: sparse_kbar_floats of scratch.
+// (blk_ld 0: packed per stream); qbar: [items][head_dim] and scores:
+// [items][n_tiles of the item's stream] fp32 scratch.
 void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32_t blk_ld,
-                           float* kbar);
-// Selection: key-tile means, then per item the scores mean(q) . mean(k) and
-// its n_keep best tiles, written ascending (padded with -1 up to blk_ld).
+                           float* qbar, float* scores);
+// Selection: per item the scores mean(q) . mean(k) of its key tiles and its
+// n_keep best tiles, written ascending (padded with -1 up to blk_ld).
 hipError_t launch_sparse_select(hipStream_t st, const AttnArgs& a, int head_dim);
 // Attention of every item over its kept tiles only.
 hipError_t launch_sparse_attention(hipStream_t st, const AttnArgs& a, int head_dim);

@@ -190,19 +190,21 @@ def test_sparsity_validation():
     assert A.ardit_workspace_size(d, A.Batch([192], [64 * 16384], sparsity=[0.0])) > 0
 
 
-def test_sparse_workspace_holds_means_and_lists():
-    """Extra workspace of a sparse batch: fp32 key-tile means (H x tiles x d)
-    plus the kept-tile lists (H x query tiles x n_keep int32), each rounded up
-    to 256 bytes; n_keep from the oracle's rule."""
+def test_sparse_workspace_holds_means_scores_and_lists():
+    """Extra workspace of a sparse batch: the fp32 mean query of every item
+    (H x query tiles x d), its fp32 score per key tile and the kept-tile lists
+    (H x query tiles x n_keep int32), each rounded up to 256 bytes; n_keep
+    from the oracle's rule."""
     from oracle.sparse_ref import keep_count
     d = _dims()
     q, c = 768, 6336                       # 3 query tiles; 7104 keys = 111 tiles
     dense = A.ardit_workspace_size(d, A.Batch([q], [c]))
     assert A.ardit_workspace_size(d, A.Batch([q], [c], sparsity=[0.0])) == dense
     up = lambda n: (n + 255) // 256 * 256
+    items = 4 * 3
     for rho in (0.6, 0.7, 0.8, 0.9, 1.0):
         nk = keep_count(111, rho)
-        want = dense + up(4 * 111 * 64 * 4) + up(4 * 3 * nk * 4)
+        want = dense + up(items * 64 * 4) + up(items * 111 * 4) + up(items * nk * 4)
         assert A.ardit_workspace_size(d, A.Batch([q], [c], sparsity=[rho])) == want, rho
 
 

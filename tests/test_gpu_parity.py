@@ -585,3 +585,27 @@ def test_sparse_block_varlen(A):
         parity(out[b * L:(b + 1) * L] - c.x[b], ref["out"] - c.x[b], f"sparse out-x stream {b}",
                tol=5e-2, quantum=ref["out"], cos_ref=bf16_round(ref["out"]) - c.x[b])
     assert checked >= 2, f"only {checked} streams had an unambiguous selection"
+
+
+def test_sparse_long_cache_more_than_1024_tiles(A):
+    """A 66860-key stream (1045 key tiles, past the 1024 the selection keeps in
+    registers) next to a short one: the lists of both match the oracle's and
+    the attention matches on sampled rows."""
+    sh = BlockShape(dim=128, n_heads=2, head_dim=64, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    q_lens, caches, rho = [300, 129], [66560, 128], [0.9, 0.7]
+    pc, dims, _, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 61)
+    batch = A.Batch(q_lens, caches, sparsity=rho)
+    H = sh.n_heads
+    rows = _sparse_rows(A, dims, batch, q, pc.kv(A), row_stride=S.keep_count(1045, 0.9))
+    _attn(A, dims, batch, q, pc.kv(A), o)
+    _sync()
+    og = host_f32(o)
+    off = r0 = 0
+    for b, n in enumerate(q_lens):
+        nq = (n + 255) // 256
+        lists = _check_selection(rows[r0:r0 + H * nq], qs[b], ks[b], rho[b], H, f"stream {b}")
+        sel = sample_rows(n, seed=b)
+        ref = S.sparse_attention(qs[b], ks[b], vs[b], lists, rows=sel).reshape(len(sel), -1)
+        parity(og[off:off + n][sel], ref, f"long sparse attn stream {b}", quantum=ref)
+        off += n
+        r0 += H * nq
