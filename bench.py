@@ -51,7 +51,10 @@ def parse():
     p.add_argument("--layers", type=int, default=LAYERS)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--sparsity", type=float, default=0.0, metavar="RHO",
-                   help="attention sparsity rho of the stream (0: dense)")
+                   help="attention sparsity rho of every stream (0: dense)")
+    p.add_argument("--workload", choices=("block13b", "ragged"), default="block13b",
+                   help="ragged: the 8-stream batch of 1.3B-class blocks (profiling of the "
+                        "elementwise kernels at 37440 rows); default 30 layers -> 4 there")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB on the device 5 times with one kernel (counter calibration)")
     return p.parse_args()
@@ -101,25 +104,36 @@ def copy_probe(mib):
 
 
 class Model:
-    """Weights, pages and text K/V of every layer, drawn on the device."""
+    """Weights, pages and text K/V of every layer for a batch of streams (one
+    chunk each, stream b over cache_lens[b] cached tokens), drawn on the device."""
 
-    def __init__(self, A, sh, n_layers, cache_len, ctx_len, dev, rho=0.0):
+    def __init__(self, A, sh, n_layers, cache_lens, ctx_len, dev, rho=0.0, timesteps=None):
         import torch
         self.A, self.sh, self.n_layers = A, sh, n_layers
         D, F, H, d = sh.dim, sh.ffn_dim, sh.n_heads, sh.head_dim
         T = sh.tokens_per_frame
-        self.cache_len, self.ctx_len = cache_len, ctx_len
-        self.frames = cache_len // T + sh.frames
+        B = len(cache_lens)
+        self.B = B
+        self.cache_lens, self.ctx_len = list(cache_lens), ctx_len
+        self.cache_len = cache_lens[0]
+        frames = [c // T + sh.frames for c in cache_lens]
+        self.frames = sum(frames)
         self.dims = A.dims_from_shape(sh)
         self.rho = rho
-        self.batch = A.Batch([sh.chunk_tokens], [cache_len], [cache_len // T], [ctx_len],
-                             sparsity=[rho])
+        self.timesteps = timesteps
+        self.batch = A.Batch([sh.chunk_tokens] * B, cache_lens, [c // T for c in cache_lens],
+                             [ctx_len] * B, sparsity=[rho] * B)
         self.ws_bytes = A.ardit_workspace_size(self.dims, self.batch)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
         from workloads.gen import block_weight_shapes, GAIN_NAMES
         shapes = block_weight_shapes(sh)
         self.w, self.kv, self.ctx_k, self.ctx_v, self.keep = [], [], [], [], []
-        self.table = torch.arange(self.frames, dtype=torch.int32, device=dev).reshape(1, -1)
+        table = torch.zeros((B, max(frames)), dtype=torch.int32)
+        first = 0
+        for b, nf in enumerate(frames):
+            table[b, :nf] = torch.arange(first, first + nf, dtype=torch.int32)
+            first += nf
+        self.table = table.to(dev)
         for layer in range(n_layers):
             g = torch.Generator(device=dev)
             g.manual_seed(15319 + 3 + 1000 * layer)
@@ -131,13 +145,13 @@ class Model:
                 wd[name] = t if name == "mod_table" else t.to(torch.bfloat16)
             kp = torch.randn((self.frames, H, T, d), generator=g, device=dev).to(torch.bfloat16)
             vp = torch.randn((self.frames, H, d, T), generator=g, device=dev).to(torch.bfloat16)
-            ctx = torch.randn((ctx_len, D), generator=g, device=dev).to(torch.bfloat16)
-            ck = torch.empty(ctx_len * D, dtype=torch.bfloat16, device=dev)
+            ctx = torch.randn((B * ctx_len, D), generator=g, device=dev).to(torch.bfloat16)
+            ck = torch.empty(B * ctx_len * D, dtype=torch.bfloat16, device=dev)
             cv = torch.empty_like(ck)
             w = A.block_weights(wd)
             A.ardit_ctx_kv(None, self.dims, self.batch, ctx, w, ck, cv, self.ws, self.ws_bytes)
             self.w.append(w)
-            self.kv.append(A.kv_paged(kp, vp, self.table, self.frames, self.frames))
+            self.kv.append(A.kv_paged(kp, vp, self.table, self.frames, max(frames)))
             self.ctx_k.append(ck)
             self.ctx_v.append(cv)
             self.keep.append((wd, kp, vp, ctx))
@@ -148,15 +162,15 @@ class Model:
         self.tw_dev = {k: (torch.randn(s, generator=g, device=dev) * 0.02).to(torch.bfloat16)
                        for k, s in tshapes.items()}
         self.tw = A.time_weights(self.tw_dev)
-        self.xs = [torch.randn((sh.chunk_tokens, D), generator=g, device=dev).to(torch.bfloat16)
+        self.xs = [torch.randn((B * sh.chunk_tokens, D), generator=g, device=dev).to(torch.bfloat16)
                    for _ in TIMESTEPS]
-        self.mod = torch.empty((1, 6, D), dtype=torch.float32, device=dev)
+        self.mod = torch.empty((B, 6, D), dtype=torch.float32, device=dev)
         self.out = torch.empty_like(self.xs[0])
 
     def step(self, k):
         A = self.A
-        A.ardit_time_mod(None, self.dims, [TIMESTEPS[k % len(TIMESTEPS)]], self.tw, self.mod,
-                         self.ws, self.ws_bytes)
+        ts = self.timesteps or [TIMESTEPS[k % len(TIMESTEPS)]] * self.B
+        A.ardit_time_mod(None, self.dims, ts, self.tw, self.mod, self.ws, self.ws_bytes)
         A.ardit_stack_fwd(None, self.dims, self.batch, self.xs[k % len(self.xs)], self.kv,
                           self.mod, self.ctx_k, self.ctx_v, self.w, self.out, self.ws,
                           self.ws_bytes)
@@ -220,11 +234,15 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    wl = WORKLOADS["block13b"]
+    wl = WORKLOADS[args.workload]
     sh = wl.shape
-    cache_len = wl.cache_chunks[0] * sh.chunk_tokens
+    cache_lens = [c * sh.chunk_tokens for c in wl.cache_chunks]
+    ragged = args.workload == "ragged"
+    if ragged and args.layers == LAYERS:
+        args.layers = 4
     log(f"drawing {args.layers} layers on the device")
-    model = Model(A, sh, args.layers, cache_len, wl.ctx_len, dev, rho=args.sparsity)
+    model = Model(A, sh, args.layers, cache_lens, wl.ctx_len, dev, rho=args.sparsity,
+                  timesteps=[float(t) for t in wl.timesteps] if ragged else None)
     torch.cuda.synchronize()
     log("warmup")
     for k in range(args.warmup):
@@ -245,22 +263,34 @@ def main():
     n_attn, attn_ms = A.ardit_timing_collect()
     ms_step = total_ms / args.steps
     ms_block = ms_step / args.layers
-    L_q, L_k, D = sh.chunk_tokens, cache_len + sh.chunk_tokens, sh.dim
-    n_tiles = (L_k + 63) // 64
-    keys = L_k
-    if args.sparsity > 0:
-        n_keep = max(1, min(n_tiles, math.ceil((1.0 - args.sparsity) * n_tiles - 1e-3)))
-        keys = min(L_k, 64 * n_keep)
-    attn_flops = 4.0 * L_q * keys * D
+    L_q, D = sh.chunk_tokens, sh.dim
+    L_k = cache_lens[0] + L_q
+    attn_flops = 0.0
+    for c in cache_lens:
+        n_tiles = (c + L_q + 63) // 64
+        keys = c + L_q
+        if args.sparsity > 0:
+            n_keep = max(1, min(n_tiles, math.ceil((1.0 - args.sparsity) * n_tiles - 1e-3)))
+            keys = min(c + L_q, 64 * n_keep)
+        attn_flops += 4.0 * L_q * keys * D
     attn_avg_ms = attn_ms / max(n_attn, 1)
     achieved = attn_flops / (attn_avg_ms * 1e-3) / 1e12
     log(f"{ms_step:.3f} ms/step, {ms_block:.4f} ms/block, attention {attn_avg_ms:.4f} ms "
         f"({achieved:.1f} TFLOP/s) over {n_attn} launches")
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not ragged:
         log("timing the CPU oracle on one block step")
         cpu = cpu_baseline(model)
         log(f"oracle: {cpu['value']} ms on {cpu['cores']} threads")
+    if ragged:
+        workload_name = ("ragged batch of 8 streams of the 1.3B-class block (D=1536, 12x128 "
+                         "heads, FFN 8960), one 4680-token chunk each over caches of "
+                         f"{'/'.join(str(c) for c in wl.cache_chunks)} chunks, 512 text tokens "
+                         f"each, {args.layers} layers, per-stream t")
+    else:
+        workload_name = ("1.3B-class AR-DiT block: D=1536, 12x128 heads, FFN 8960, chunk 4680 "
+                         "tokens (3x30x52) over a 28080-token cache, 512 text tokens, "
+                         f"{args.layers} layers, t=1000/750/500/250")
     line = {
         "metric": "ms per chunk-denoise-step per block",
         "value": round(ms_block, 4),
@@ -274,15 +304,14 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded normal draws, random-init weights)",
-        "config": {"workload": "1.3B-class AR-DiT block: D=1536, 12x128 heads, FFN 8960, "
-                               "chunk 4680 tokens (3x30x52) over a 28080-token cache, "
-                               "512 text tokens, 30 layers, t=1000/750/500/250",
-                   "layers": args.layers, "chunk_tokens": L_q, "kv_tokens": L_k,
+        "config": {"workload": workload_name,
+                   "layers": args.layers, "chunk_tokens": L_q,
+                   "kv_tokens": L_k if not ragged else [c + L_q for c in cache_lens],
                    "ctx_tokens": wl.ctx_len, "sparsity": args.sparsity,
-                   "attended_keys": keys},
+                   "attended_keys": keys if not ragged else None},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None if args.sparsity else measured_traffic(),
+                     "traffic": None if (args.sparsity or ragged) else measured_traffic(),
                      "kernel": ("block-sparse paged self-attention" if args.sparsity
                                 else "paged self-attention"),
                      "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},

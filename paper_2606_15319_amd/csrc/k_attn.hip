@@ -30,6 +30,8 @@
 // kernel merges.
 #include <math.h>
 
+#include <vector>
+
 #include "launch.h"
 
 namespace ardit {
@@ -463,10 +465,12 @@ __global__ __launch_bounds__(NTHR, 1) void attn_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * KLD];
   __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * VLD];
 
-  // ---- work item (XCD-aware: consecutive items share an XCD and its L2)
+  // ---- work item (XCD-aware: each XCD runs a contiguous range of items, so
+  // the items of one head share its L2, the ranges balanced by tile count)
   const int pid = blockIdx.x;
-  const int L = (pid % kNumXcd) * a.per_xcd + pid / kNumXcd;
-  if (L >= a.total_items) return;
+  const int xcd = pid % kNumXcd;
+  const int L = a.xcd_begin[xcd] + pid / kNumXcd;
+  if (L >= a.xcd_begin[xcd + 1]) return;
   int si = 0;
   for (int i = 1; i < a.n_streams; ++i)
     if (L >= a.s[i].item_begin) si = i;
@@ -813,8 +817,9 @@ __global__ __launch_bounds__(NTHR, 1) void attn_sparse_kernel(const AttnArgs a) 
   __shared__ __attribute__((aligned(16))) bf16_t sK[2][BKV * HD];
   __shared__ __attribute__((aligned(16))) bf16_t sV[2][HD * BKV];
   const int pid = blockIdx.x;
-  const int L = (pid % kNumXcd) * a.per_xcd + pid / kNumXcd;
-  if (L >= a.total_items) return;
+  const int xcd = pid % kNumXcd;
+  const int L = a.xcd_begin[xcd] + pid / kNumXcd;
+  if (L >= a.xcd_begin[xcd + 1]) return;
   int si = 0;
   for (int i = 1; i < a.n_streams; ++i)
     if (L >= a.s[i].item_begin) si = i;
@@ -839,6 +844,108 @@ hipError_t launch_sparse_attention(hipStream_t st, const AttnArgs& a, int head_d
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+namespace {
+
+constexpr int kCusPerXcd = 32;   // MI355X: 8 XCDs of 32 CUs
+
+// List schedule of item costs [i, n) (plan order) onto one XCD's CUs, each CU
+// taking the next item when it frees (how the dispatcher hands out an XCD's
+// workgroups in order, one 512-thread workgroup per CU).  Returns the first
+// item past those that finish by makespan M; with share > 0 it also stops once
+// the XCD's cost reaches share.
+int fill_xcd(const int32_t* cost, int i, int n, int64_t M, int64_t share) {
+  int64_t fin[kCusPerXcd] = {};
+  int64_t taken = 0;
+  for (; i < n; ++i) {
+    if (share > 0 && taken >= share) break;
+    int k = 0;
+    for (int c = 1; c < kCusPerXcd; ++c) k = fin[c] < fin[k] ? c : k;
+    if (fin[k] + cost[i] > M) break;
+    fin[k] += cost[i];
+    taken += cost[i];
+  }
+  return i;
+}
+
+// Contiguous split of the items over the XCDs that minimises the makespan of
+// the slowest XCD under list scheduling (binary search on the makespan), with
+// the items spread evenly by cost where that makespan allows.
+void split_by_makespan(const int32_t* cost, int n, int64_t total, int32_t* begin) {
+  int64_t lo = 0, hi = total;
+  for (int i = 0; i < n; ++i) lo = cost[i] > lo ? cost[i] : lo;
+  auto feasible = [&](int64_t M) {
+    int i = 0;
+    for (int x = 0; x < kNumXcd && i < n; ++x) i = fill_xcd(cost, i, n, M, 0);
+    return i == n;
+  };
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    if (feasible(mid)) hi = mid;
+    else lo = mid + 1;
+  }
+  // even spread first, bounded by the makespan; the greedy fill if that fails
+  for (int pass = 0; pass < 2; ++pass) {
+    int i = 0;
+    int64_t done = 0;
+    begin[0] = 0;
+    for (int x = 0; x < kNumXcd; ++x) {
+      int64_t share = 0;
+      if (pass == 0 && x < kNumXcd - 1) {
+        share = (total - done) / (kNumXcd - x);
+        share = share > 0 ? share : 1;
+      }
+      const int e = fill_xcd(cost, i, n, lo, share);
+      for (int j = i; j < e; ++j) done += cost[j];
+      i = e;
+      begin[x + 1] = i;
+    }
+    if (i == n) return;
+  }
+}
+
+// The last plan's XCD split, reused while the item costs repeat (every layer
+// and denoising step of a chunk has the same geometry).
+struct XcdSplitCache {
+  std::vector<int32_t> key;
+  int32_t begin[kNumXcd + 1];
+};
+
+}  // namespace
+
+void balance_items_over_xcds(AttnArgs& a, bool sparse) {
+  // per-item cost in plan order, compressed per stream for the cache key
+  thread_local XcdSplitCache cache;
+  std::vector<int32_t> key;
+  key.reserve(2 * a.n_streams + 1);
+  key.push_back(a.H);
+  int64_t total = 0;
+  for (int i = 0; i < a.n_streams; ++i) {
+    const int32_t c = sparse ? a.s[i].n_keep : a.s[i].n_tiles;
+    key.push_back(a.s[i].n_qtiles);
+    key.push_back(c);
+    total += static_cast<int64_t>(a.s[i].n_qtiles) * a.H * c;
+  }
+  const int n = a.total_items;
+  if (key != cache.key) {
+    if (n <= 65536) {
+      std::vector<int32_t> cost(n);
+      for (int i = 0; i < a.n_streams; ++i)
+        for (int j = 0; j < a.s[i].n_qtiles * a.H; ++j)
+          cost[a.s[i].item_begin + j] = sparse ? a.s[i].n_keep : a.s[i].n_tiles;
+      split_by_makespan(cost.data(), n, total, cache.begin);
+    } else {   // very large batches: equal item counts
+      for (int x = 0; x <= kNumXcd; ++x)
+        cache.begin[x] = static_cast<int32_t>(static_cast<int64_t>(n) * x / kNumXcd);
+    }
+    cache.key = key;
+  }
+  int most = 0;
+  for (int x = 0; x <= kNumXcd; ++x) a.xcd_begin[x] = cache.begin[x];
+  for (int x = 0; x < kNumXcd; ++x)
+    most = a.xcd_begin[x + 1] - a.xcd_begin[x] > most ? a.xcd_begin[x + 1] - a.xcd_begin[x] : most;
+  a.per_xcd = most;
 }
 
 size_t attention_split_bytes(int head_dim) {
@@ -878,7 +985,6 @@ void plan_attention(AttnArgs& a, int head_dim, float* split_ws) {
   a.split_tiles = 0;
   a.part_o = nullptr;
   a.part_ml = nullptr;
-  a.per_xcd = (items + kNumXcd - 1) / kNumXcd;
   // Split when the items fit one round of workgroups but leave more than a
   // quarter of them idle: every item keeps its first W tiles (W = the even
   // share of all tiles per workgroup) and the idle workgroups take equal ranges
@@ -908,6 +1014,7 @@ void plan_attention(AttnArgs& a, int head_dim, float* split_ws) {
     }
   }
   for (int i = 0; i < n; ++i) a.s[i] = tmp[i];
+  if (!a.split_blocks) balance_items_over_xcds(a, false);
 }
 
 template <int HD, bool P, bool V>

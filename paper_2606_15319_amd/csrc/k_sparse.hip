@@ -334,7 +334,7 @@ void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32
   }
   a.n_streams = n;
   a.total_items = items;
-  a.per_xcd = (items + kNumXcd - 1) / kNumXcd;
+  balance_items_over_xcds(a, true);
   a.split_blocks = 0;
   a.total_tiles = 0;
   a.split_tiles = 0;

@@ -77,7 +77,9 @@ struct AttnArgs {
   float scale_log2;    // log2(e) / sqrt(d)
   int32_t n_streams;
   int32_t total_items;
-  int32_t per_xcd;
+  int32_t per_xcd;       // workgroups per XCD (grid = per_xcd * kNumXcd)
+  int32_t xcd_begin[kNumXcd + 1];  // one workgroup per item: XCD x runs items
+                                   // [xcd_begin[x], xcd_begin[x + 1]), in order
   int32_t split_blocks;  // 0: one workgroup per item; else the workgroups of a split schedule
   int32_t total_tiles;   // split: tail tiles of all items, concatenated
   int32_t split_tiles;   // split: tail tiles per spare workgroup
@@ -92,6 +94,11 @@ struct AttnArgs {
 };
 static_assert(sizeof(AttnArgs) <= 4096, "attention arguments must fit the kernel-argument buffer");
 
+// Splits the planned items (streams in order, n_qtiles * H items each, costing
+// n_keep tiles each when sparse, else n_tiles) into kNumXcd contiguous ranges
+// of equal total cost: xcd_begin and per_xcd.  Contiguous ranges keep the
+// items of one head on one XCD, sharing its L2.
+void balance_items_over_xcds(AttnArgs& a, bool sparse);
 // Device bytes of the partial results of a split schedule.
 size_t attention_split_bytes(int head_dim);
 // Fills the schedule fields from the streams' lengths, ordering streams by
