@@ -2,9 +2,10 @@
 // QK-RMSNorm + 3D RoPE + key append, value append (transposed pages), text
 // key/value layout, and the small time-modulation MLP.
 //
-// One 64-lane wave owns one token row: 16-byte loads/stores, fp32 math, a
-// wave reduction for the mean square.  Rows of up to 8192 elements are held
-// in registers so each row is read from HBM once.
+// One 64-lane wave owns a token row at a time: 16-byte loads/stores, fp32
+// math, a wave reduction for the mean square.  Rows of up to 8192 elements
+// are held in registers so each row is read from HBM once; vectors shared by
+// a workgroup's rows (modulation, gains, rotation terms) are staged in LDS.
 #include <math.h>
 
 #include "launch.h"
@@ -25,115 +26,174 @@ __device__ __forceinline__ void load8(const float* p, float* f) {
   f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
 }
 
-// One wave per row; a lane holds chunks lane + 64 i (i < MAXC) of 8 elements.
+// A workgroup of 4 waves handles kRowsPerGroup consecutive rows, 2 per wave;
+// the per-row vectors it shares (modulation, gains) are staged once in LDS as
+// fp32.  A lane holds chunks lane + 64 i (i < MAXC) of 8 elements of each of
+// its rows, so every row is read from HBM once and all its loads are in
+// flight together.
+constexpr int kRowsPerGroup = 8;
+constexpr int kRowsPerWave = kRowsPerGroup / 4;
+
+// y = rms(x) * (1 + scale) + shift with scale = mod[b][scale_row] +
+// mod_table[scale_row] and shift likewise.  Streams hold rows_per_stream
+// rows, a multiple of kRowsPerGroup, so a workgroup's rows share one stream.
 template <typename T, int MAXC>
 __global__ __launch_bounds__(256) void adaln_norm_kernel(
     const T* __restrict__ x, bf16_t* __restrict__ out, int N, int D,
     const float* __restrict__ mod, const float* __restrict__ mod_table, int shift_row,
     int scale_row, int rows_per_stream, float eps) {
+  extern __shared__ float4 lds_mod[];   // D / 4 of (1 + scale), then D / 4 of shift
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= N) return;
-  const int b = row / rows_per_stream;
+  const int row0 = blockIdx.x * kRowsPerGroup + (threadIdx.x >> 6) * kRowsPerWave;
   const int nchunk = D >> 3;
-  const T* xr = x + static_cast<size_t>(row) * D;
-  float v[MAXC][8];
-  float ss = 0.f;
+  // this wave's rows, loads issued before the modulation is staged
+  float v[kRowsPerWave][MAXC][8];
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = lane + 64 * i;
-    if (c < nchunk) {
-      load8(xr + 8 * c, v[i]);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const T* xr = x + static_cast<size_t>(min(row0 + r, N - 1)) * D;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) load8(xr + 8 * c, v[r][i]);
     }
   }
-  ss = wave_sum(ss);
-  const float r = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
-  const float* msh = mod + (static_cast<size_t>(b) * 6 + shift_row) * D;
-  const float* msc = mod + (static_cast<size_t>(b) * 6 + scale_row) * D;
-  const float* tsh = mod_table + static_cast<size_t>(shift_row) * D;
-  const float* tsc = mod_table + static_cast<size_t>(scale_row) * D;
-  uint4* orow = reinterpret_cast<uint4*>(out + static_cast<size_t>(row) * D);
+  {
+    const int b = (blockIdx.x * kRowsPerGroup) / rows_per_stream;
+    const float4* msh = reinterpret_cast<const float4*>(mod + (static_cast<size_t>(b) * 6 + shift_row) * D);
+    const float4* msc = reinterpret_cast<const float4*>(mod + (static_cast<size_t>(b) * 6 + scale_row) * D);
+    const float4* tsh = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(shift_row) * D);
+    const float4* tsc = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(scale_row) * D);
+    for (int k = threadIdx.x; k < D / 4; k += 256) {
+      const float4 a = msc[k], c = tsc[k], sh = msh[k], th = tsh[k];
+      lds_mod[k] = make_float4(1.f + a.x + c.x, 1.f + a.y + c.y, 1.f + a.z + c.z, 1.f + a.w + c.w);
+      lds_mod[D / 4 + k] = make_float4(sh.x + th.x, sh.y + th.y, sh.z + th.z, sh.w + th.w);
+    }
+  }
+  __syncthreads();
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = lane + 64 * i;
-    if (c < nchunk) {
-      float sh[8], sc[8], th[8], tc[8], y[8];
-      load8(msh + 8 * c, sh);
-      load8(msc + 8 * c, sc);
-      load8(tsh + 8 * c, th);
-      load8(tsc + 8 * c, tc);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const int row = row0 + r;
+    float ss = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = v[i][e] * r * (1.0f + sc[e] + tc[e]) + (sh[e] + th[e]);
-      orow[c] = pack8(y);
+    for (int i = 0; i < MAXC; ++i)
+      if (lane + 64 * i < nchunk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += v[r][i][e] * v[r][i][e];
+    ss = wave_sum(ss);
+    const float rs = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
+    if (row >= N) continue;
+    uint4* orow = reinterpret_cast<uint4*>(out + static_cast<size_t>(row) * D);
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) {
+        const float4 a0 = lds_mod[2 * c], a1 = lds_mod[2 * c + 1];
+        const float4 b0 = lds_mod[D / 4 + 2 * c], b1 = lds_mod[D / 4 + 2 * c + 1];
+        const float sa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        const float sb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = v[r][i][e] * rs * sa[e] + sb[e];
+        orow[c] = pack8(y);
+      }
     }
   }
 }
 
+// y = rms(x) * gain, the gain staged in LDS as fp32.
 template <typename T, int MAXC>
 __global__ __launch_bounds__(256) void rms_gain_kernel(const T* in, bf16_t* out, int N, int D,
                                                         const bf16_t* __restrict__ gain,
                                                         float eps) {
+  extern __shared__ float4 lds_gain[];   // D / 4
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= N) return;
+  const int row0 = blockIdx.x * kRowsPerGroup + (threadIdx.x >> 6) * kRowsPerWave;
   const int nchunk = D >> 3;
-  const T* xr = in + static_cast<size_t>(row) * D;
-  float v[MAXC][8];
-  float ss = 0.f;
+  float v[kRowsPerWave][MAXC][8];
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = lane + 64 * i;
-    if (c < nchunk) {
-      load8(xr + 8 * c, v[i]);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const T* xr = in + static_cast<size_t>(min(row0 + r, N - 1)) * D;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) load8(xr + 8 * c, v[r][i]);
     }
   }
-  ss = wave_sum(ss);
-  const float r = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
-  uint4* orow = reinterpret_cast<uint4*>(out + static_cast<size_t>(row) * D);
+  for (int k = threadIdx.x; k < D / 8; k += 256) {
+    float g[8];
+    load8(gain + 8 * k, g);
+    lds_gain[2 * k] = make_float4(g[0], g[1], g[2], g[3]);
+    lds_gain[2 * k + 1] = make_float4(g[4], g[5], g[6], g[7]);
+  }
+  __syncthreads();
 #pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = lane + 64 * i;
-    if (c < nchunk) {
-      float g[8], y[8];
-      load8(gain + 8 * c, g);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const int row = row0 + r;
+    float ss = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = v[i][e] * r * g[e];
-      orow[c] = pack8(y);
+    for (int i = 0; i < MAXC; ++i)
+      if (lane + 64 * i < nchunk)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss += v[r][i][e] * v[r][i][e];
+    ss = wave_sum(ss);
+    const float rs = 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
+    if (row >= N) continue;
+    uint4* orow = reinterpret_cast<uint4*>(out + static_cast<size_t>(row) * D);
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) {
+        const float4 g0 = lds_gain[2 * c], g1 = lds_gain[2 * c + 1];
+        const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = v[r][i][e] * rs * g[e];
+        orow[c] = pack8(y);
+      }
     }
   }
 }
 
-// chunks per lane needed for a row of D elements, rounded up to 1, 2, 4, 8, 16
+// chunks per lane needed for a row of D elements, rounded up to a size that
+// has an instantiation (the row arrays are sized by it)
 static int row_chunks(int D) {
   const int c = (D / 8 + 63) / 64;
-  return c <= 1 ? 1 : c <= 2 ? 2 : c <= 4 ? 4 : c <= 8 ? 8 : 16;
+  const int sizes[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16};
+  for (int s : sizes)
+    if (c <= s) return s;
+  return 16;
 }
 
-#define ARDIT_ROW_DISPATCH(KERNEL, T, ...)                                              \
-  switch (row_chunks(D)) {                                                              \
-    case 1: hipLaunchKernelGGL((KERNEL<T, 1>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
-    case 2: hipLaunchKernelGGL((KERNEL<T, 2>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
-    case 4: hipLaunchKernelGGL((KERNEL<T, 4>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
-    case 8: hipLaunchKernelGGL((KERNEL<T, 8>), grid, dim3(256), 0, st, __VA_ARGS__); break;  \
-    default: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(256), 0, st, __VA_ARGS__); break; \
+#define ARDIT_ROW_CASE(KERNEL, T, C, LDS, ...) \
+  case C: hipLaunchKernelGGL((KERNEL<T, C>), grid, dim3(256), LDS, st, __VA_ARGS__); break;
+#define ARDIT_ROW_DISPATCH(KERNEL, T, LDS, ...)         \
+  switch (row_chunks(D)) {                              \
+    ARDIT_ROW_CASE(KERNEL, T, 1, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 2, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 3, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 4, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 5, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 6, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 8, LDS, __VA_ARGS__)      \
+    ARDIT_ROW_CASE(KERNEL, T, 10, LDS, __VA_ARGS__)     \
+    ARDIT_ROW_CASE(KERNEL, T, 12, LDS, __VA_ARGS__)     \
+    default: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(256), LDS, st, __VA_ARGS__); break; \
   }
 
 hipError_t launch_adaln_norm(hipStream_t st, const void* x, bool x_f32, bf16_t* out, int N, int D,
                              const float* mod, const float* mod_table, int shift_row,
                              int scale_row, int rows_per_stream, float eps) {
   if (N == 0) return hipSuccess;
-  const dim3 grid((N + 3) / 4);
+  if (rows_per_stream % kRowsPerGroup != 0) return hipErrorInvalidValue;
+  const dim3 grid((N + kRowsPerGroup - 1) / kRowsPerGroup);
+  const size_t lds = 2 * sizeof(float) * D;
   if (x_f32) {
     const float* xf = static_cast<const float*>(x);
-    ARDIT_ROW_DISPATCH(adaln_norm_kernel, float, xf, out, N, D, mod, mod_table, shift_row,
+    ARDIT_ROW_DISPATCH(adaln_norm_kernel, float, lds, xf, out, N, D, mod, mod_table, shift_row,
                        scale_row, rows_per_stream, eps);
   } else {
     const bf16_t* xb = static_cast<const bf16_t*>(x);
-    ARDIT_ROW_DISPATCH(adaln_norm_kernel, bf16_t, xb, out, N, D, mod, mod_table, shift_row,
+    ARDIT_ROW_DISPATCH(adaln_norm_kernel, bf16_t, lds, xb, out, N, D, mod, mod_table, shift_row,
                        scale_row, rows_per_stream, eps);
   }
   return hipGetLastError();
@@ -142,13 +202,14 @@ hipError_t launch_adaln_norm(hipStream_t st, const void* x, bool x_f32, bf16_t* 
 hipError_t launch_rms_gain(hipStream_t st, const void* in, bool in_f32, bf16_t* out, int N, int D,
                            const bf16_t* gain, float eps) {
   if (N == 0) return hipSuccess;
-  const dim3 grid((N + 3) / 4);
+  const dim3 grid((N + kRowsPerGroup - 1) / kRowsPerGroup);
+  const size_t lds = sizeof(float) * D;
   if (in_f32) {
     const float* xf = static_cast<const float*>(in);
-    ARDIT_ROW_DISPATCH(rms_gain_kernel, float, xf, out, N, D, gain, eps);
+    ARDIT_ROW_DISPATCH(rms_gain_kernel, float, lds, xf, out, N, D, gain, eps);
   } else {
     const bf16_t* xb = static_cast<const bf16_t*>(in);
-    ARDIT_ROW_DISPATCH(rms_gain_kernel, bf16_t, xb, out, N, D, gain, eps);
+    ARDIT_ROW_DISPATCH(rms_gain_kernel, bf16_t, lds, xb, out, N, D, gain, eps);
   }
   return hipGetLastError();
 }
@@ -180,95 +241,129 @@ __device__ __forceinline__ int clamp_page(int p, int n_pages) {
   return p < 0 ? 0 : (p >= n_pages ? n_pages - 1 : p);
 }
 
+// A workgroup handles kRowsPerGroup rows, 2 per wave.  Per row, lane k < d/2
+// computes the rotation (cos, sin) of pair k, shared through LDS; the gains
+// are staged in LDS as fp32; both rows' q and k are loaded before any math.
+template <int MAXC>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p) {
+  extern __shared__ float4 lds_qk[];   // g_q (D / 4), g_k (D / 4), then cos / sin per row
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= p.N) return;
-  const int b = find_stream(p.rs, row);
-  const RowStream s = p.rs.s[b];
-  const int t = row - s.row_begin;
-  const int f = static_cast<int>(fdiv(static_cast<uint32_t>(t), p.fT));
-  const int rem = t - f * p.T;
-  const int i = static_cast<int>(fdiv(static_cast<uint32_t>(rem), p.fW));
-  const int j = rem - i * p.lat_w;
-
-  // this lane's rotation: pair `lane` of a head (lanes >= hd/2 unused)
-  float cs = 1.f, sn = 0.f;
-  if (lane < (p.hd >> 1)) {
-    const int pos = lane < p.pairs_t ? s.frame_pos0 + f : (lane < p.pairs_t + p.pairs_h ? i : j);
-    sincosf(static_cast<float>(pos) * p.inv_freq[lane], &sn, &cs);
-  }
-
+  const int wave = threadIdx.x >> 6;
+  const int row0 = blockIdx.x * kRowsPerGroup + wave * kRowsPerWave;
   const int nchunk = p.D >> 3;
-  const uint4* qr = reinterpret_cast<const uint4*>(p.qkv + static_cast<size_t>(row) * 3 * p.D);
-  const uint4* kr = qr + nchunk;
-  uint4 qraw[kMaxChunksPerLane], kraw[kMaxChunksPerLane];
-  float sq = 0.f, sk = 0.f;
+  float4* lg_q = lds_qk;
+  float4* lg_k = lds_qk + p.D / 4;
+  float* lcs = reinterpret_cast<float*>(lds_qk + p.D / 2);   // [kRowsPerGroup][64]
+  float* lsn = lcs + kRowsPerGroup * 64;
+
+  uint4 qraw[kRowsPerWave][MAXC], kraw[kRowsPerWave][MAXC];
 #pragma unroll
-  for (int c8 = 0; c8 < kMaxChunksPerLane; ++c8) {
-    const int c = lane + 64 * c8;
-    if (c < nchunk) {
-      qraw[c8] = qr[c];
-      kraw[c8] = kr[c];
-      float a[8], bb[8];
-      unpack8(qraw[c8], a);
-      unpack8(kraw[c8], bb);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const uint4* qr = reinterpret_cast<const uint4*>(
+        p.qkv + static_cast<size_t>(min(row0 + r, p.N - 1)) * 3 * p.D);
+    const uint4* kr = qr + nchunk;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sq += a[e] * a[e];
-        sk += bb[e] * bb[e];
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) {
+        qraw[r][i] = qr[c];
+        kraw[r][i] = kr[c];
       }
     }
   }
-  sq = wave_sum(sq);
-  sk = wave_sum(sk);
-  const float rq = 1.0f / sqrtf(sq / static_cast<float>(p.D) + p.eps);
-  const float rk = 1.0f / sqrtf(sk / static_cast<float>(p.D) + p.eps);
-
-  const int slot = s.cache_len + t;
-  const int fr = static_cast<int>(fdiv(static_cast<uint32_t>(slot), p.fT));
-  const int page = clamp_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr],
-                              p.n_pages);
-  const int off = slot - fr * p.T;
-  const uint4* gq = reinterpret_cast<const uint4*>(p.g_q);
-  const uint4* gk = reinterpret_cast<const uint4*>(p.g_k);
-  uint4* qo = reinterpret_cast<uint4*>(p.q_out + static_cast<size_t>(row) * p.D);
+  for (int k = threadIdx.x; k < p.D / 8; k += 256) {
+    float g[8];
+    unpack8(reinterpret_cast<const uint4*>(p.g_q)[k], g);
+    lg_q[2 * k] = make_float4(g[0], g[1], g[2], g[3]);
+    lg_q[2 * k + 1] = make_float4(g[4], g[5], g[6], g[7]);
+    unpack8(reinterpret_cast<const uint4*>(p.g_k)[k], g);
+    lg_k[2 * k] = make_float4(g[0], g[1], g[2], g[3]);
+    lg_k[2 * k + 1] = make_float4(g[4], g[5], g[6], g[7]);
+  }
+  // rotation of pair `lane` of a head for each of this wave's rows
 #pragma unroll
-  for (int c8 = 0; c8 < kMaxChunksPerLane; ++c8) {
-    if (64 * c8 >= nchunk) break;  // wave-uniform
-    const int c = lane + 64 * c8;
-    // every lane takes part in the shuffles, so the per-lane guard sits inside
-    const int cc = c < nchunk ? c : 0;
-    const int e0 = (8 * cc) % p.hd;
-    const int h = (8 * cc) / p.hd;
-    const int pb = e0 >> 1;
-    float cv[4], sv[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      cv[e] = __shfl(cs, pb + e, 64);
-      sv[e] = __shfl(sn, pb + e, 64);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const int row = min(row0 + r, p.N - 1);
+    const RowStream s = p.rs.s[find_stream(p.rs, row)];
+    const int t = row - s.row_begin;
+    const int f = static_cast<int>(fdiv(static_cast<uint32_t>(t), p.fT));
+    const int rem = t - f * p.T;
+    const int i = static_cast<int>(fdiv(static_cast<uint32_t>(rem), p.fW));
+    const int j = rem - i * p.lat_w;
+    float cs = 1.f, sn = 0.f;
+    if (lane < (p.hd >> 1)) {
+      const int pos = lane < p.pairs_t ? s.frame_pos0 + f : (lane < p.pairs_t + p.pairs_h ? i : j);
+      sincosf(static_cast<float>(pos) * p.inv_freq[lane], &sn, &cs);
     }
-    if (c < nchunk) {
-      float a[8], g[8], y[8];
-      unpack8(qraw[c8], a);
-      unpack8(gq[c], g);
+    lcs[(wave * kRowsPerWave + r) * 64 + lane] = cs;
+    lsn[(wave * kRowsPerWave + r) * 64 + lane] = sn;
+  }
+  __syncthreads();
+
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x0 = a[2 * e] * rq * g[2 * e], x1 = a[2 * e + 1] * rq * g[2 * e + 1];
-        y[2 * e] = x0 * cv[e] - x1 * sv[e];
-        y[2 * e + 1] = x0 * sv[e] + x1 * cv[e];
-      }
-      qo[c] = pack8(y);
-      unpack8(kraw[c8], a);
-      unpack8(gk[c], g);
+  for (int r = 0; r < kRowsPerWave; ++r) {
+    const int row = row0 + r;
+    float sq = 0.f, sk = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x0 = a[2 * e] * rk * g[2 * e], x1 = a[2 * e + 1] * rk * g[2 * e + 1];
-        y[2 * e] = x0 * cv[e] - x1 * sv[e];
-        y[2 * e + 1] = x0 * sv[e] + x1 * cv[e];
+    for (int i = 0; i < MAXC; ++i) {
+      if (lane + 64 * i < nchunk) {
+        float a[8], bb[8];
+        unpack8(qraw[r][i], a);
+        unpack8(kraw[r][i], bb);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sq += a[e] * a[e];
+          sk += bb[e] * bb[e];
+        }
       }
-      bf16_t* dst = p.k_pages + ((static_cast<size_t>(page) * p.H + h) * p.T + off) * p.hd + e0;
-      *reinterpret_cast<uint4*>(dst) = pack8(y);
+    }
+    sq = wave_sum(sq);
+    sk = wave_sum(sk);
+    if (row >= p.N) continue;
+    const float rq = 1.0f / sqrtf(sq / static_cast<float>(p.D) + p.eps);
+    const float rk = 1.0f / sqrtf(sk / static_cast<float>(p.D) + p.eps);
+    const int b = find_stream(p.rs, row);
+    const RowStream s = p.rs.s[b];
+    const int slot = s.cache_len + row - s.row_begin;
+    const int fr = static_cast<int>(fdiv(static_cast<uint32_t>(slot), p.fT));
+    const int page = clamp_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr],
+                                p.n_pages);
+    const int off = slot - fr * p.T;
+    const float* rcs = lcs + (wave * kRowsPerWave + r) * 64;
+    const float* rsn = lsn + (wave * kRowsPerWave + r) * 64;
+    uint4* qo = reinterpret_cast<uint4*>(p.q_out + static_cast<size_t>(row) * p.D);
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nchunk) {
+        const int e0 = (8 * c) % p.hd;
+        const int h = (8 * c) / p.hd;
+        const float4 cv = *reinterpret_cast<const float4*>(rcs + (e0 >> 1));
+        const float4 sv = *reinterpret_cast<const float4*>(rsn + (e0 >> 1));
+        const float cc[4] = {cv.x, cv.y, cv.z, cv.w}, ss[4] = {sv.x, sv.y, sv.z, sv.w};
+        float a[8], y[8];
+        const float4 g0 = lg_q[2 * c], g1 = lg_q[2 * c + 1];
+        const float gq[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        unpack8(qraw[r][i], a);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x0 = a[2 * e] * rq * gq[2 * e], x1 = a[2 * e + 1] * rq * gq[2 * e + 1];
+          y[2 * e] = x0 * cc[e] - x1 * ss[e];
+          y[2 * e + 1] = x0 * ss[e] + x1 * cc[e];
+        }
+        qo[c] = pack8(y);
+        const float4 k0 = lg_k[2 * c], k1 = lg_k[2 * c + 1];
+        const float gk[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+        unpack8(kraw[r][i], a);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x0 = a[2 * e] * rk * gk[2 * e], x1 = a[2 * e + 1] * rk * gk[2 * e + 1];
+          y[2 * e] = x0 * cc[e] - x1 * ss[e];
+          y[2 * e + 1] = x0 * ss[e] + x1 * cc[e];
+        }
+        bf16_t* dst = p.k_pages + ((static_cast<size_t>(page) * p.H + h) * p.T + off) * p.hd + e0;
+        *reinterpret_cast<uint4*>(dst) = pack8(y);
+      }
     }
   }
 }
@@ -307,7 +402,16 @@ hipError_t launch_qk_norm_rope(hipStream_t st, const bf16_t* qkv, int N, const R
       p.inv_freq[pair++] =
           static_cast<float>(pow(static_cast<double>(g.theta), -2.0 * k / segs[a]));
   p.rs = rs;
-  hipLaunchKernelGGL(qk_norm_rope_kernel, dim3((N + 3) / 4), dim3(256), 0, st, p);
+  const dim3 grid((N + kRowsPerGroup - 1) / kRowsPerGroup);
+  const size_t lds = 2 * sizeof(float) * g.D + 2 * sizeof(float) * kRowsPerGroup * 64;
+  switch (row_chunks(g.D)) {
+#define ARDIT_QK_CASE(C) \
+    case C: hipLaunchKernelGGL(qk_norm_rope_kernel<C>, grid, dim3(256), lds, st, p); break;
+    ARDIT_QK_CASE(1) ARDIT_QK_CASE(2) ARDIT_QK_CASE(3) ARDIT_QK_CASE(4) ARDIT_QK_CASE(5)
+    ARDIT_QK_CASE(6) ARDIT_QK_CASE(8) ARDIT_QK_CASE(10) ARDIT_QK_CASE(12)
+#undef ARDIT_QK_CASE
+    default: hipLaunchKernelGGL(qk_norm_rope_kernel<16>, grid, dim3(256), lds, st, p); break;
+  }
   return hipGetLastError();
 }
 
