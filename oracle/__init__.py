@@ -19,3 +19,4 @@ from .ardit_ref import (  # noqa: F401
     context_kv, block_forward, full_sequence_forward,
 )
 from . import sparse_ref  # noqa: F401
+from . import fp8_ref  # noqa: F401

@@ -552,3 +552,93 @@ def test_sparse_block_forward_keeping_every_block_is_dense():
     o, blocks = S.sparse_self_attention(q, K, V, 0.5, q_block=4, k_block=4)
     assert blocks.shape == (sh.n_heads, 2, 2)
     assert not np.allclose(o, O.attention(q, K, V))
+
+
+# --------------------------------------------------------------------------
+# FP8 attention (quantisation knob Q): E4M3 rounding, microscaled blocks, bound
+# --------------------------------------------------------------------------
+F8 = O.fp8_ref
+
+
+def test_e4m3_values_and_rounding():
+    vals = F8.e4m3_values()
+    assert len(vals) == 254 and vals.max() == 448.0 and vals.min() == -448.0
+    pos = np.unique(vals[vals > 0])
+    assert pos[0] == 2.0 ** -9 and len(pos) == 126           # 7 subnormals + 15 binades x 8 - 1
+    np.testing.assert_array_equal(F8.e4m3_round(vals), vals)  # every value rounds to itself
+    # midpoints go to the even mantissa, anything past a midpoint goes up
+    def mantissa(v):
+        if v < 2.0 ** -6:
+            return int(round(v / 2.0 ** -9))
+        E = math.floor(math.log2(v))
+        return int(round(v / 2.0 ** (E - 3))) - 8
+    for lo, hi in zip(pos[:-1], pos[1:]):
+        mid = (lo + hi) / 2
+        even = lo if mantissa(lo) % 2 == 0 else hi
+        assert float(F8.e4m3_round(mid)) == even
+        assert float(F8.e4m3_round(-mid)) == -even
+        assert float(F8.e4m3_round(np.nextafter(mid, np.inf))) == hi
+        assert float(F8.e4m3_round(np.nextafter(mid, -np.inf))) == lo
+    # worked ties: 1.0625 = 1 + 1/16 lies halfway between 1 (mantissa 000) and
+    # 1.125 (001): even is 1.0; 1.1875 halfway between 1.125 (001) and 1.25 (010): 1.25
+    assert float(F8.e4m3_round(1.0625)) == 1.0 and float(F8.e4m3_round(1.1875)) == 1.25
+    assert float(F8.e4m3_round(2.0 ** -10)) == 0.0 and float(F8.e4m3_round(3 * 2.0 ** -10)) == 2.0 ** -8
+    with pytest.raises(ValueError):
+        F8.e4m3_round(464.0)
+
+
+def test_mx_block_exponent_and_landing():
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((5, 96)) * np.exp(rng.uniform(-8, 8, (5, 1)))
+    codes, e = F8.mx_quantize(x, axis=1)
+    for r in range(5):
+        for b in range(3):
+            blk = x[r, 32 * b:32 * b + 32]
+            amax = np.abs(blk).max()
+            assert e[r, 32 * b] == math.floor(math.log2(amax)) - 7
+            assert 128.0 <= np.abs(codes[r, 32 * b:32 * b + 32]).max() < 256.0
+    deq = F8.mx_dequantize(codes, e)
+    # half an E4M3 step: 2^-4 relative in the normal range, 2^-10 2^e below it
+    assert np.all(np.abs(deq - x) <= np.maximum(2.0 ** -4 * np.abs(x), np.ldexp(2.0 ** -10, e)))
+    # power-of-two scaling moves the exponent only
+    c2, e2 = F8.mx_quantize(x * 2.0 ** 5, axis=1)
+    np.testing.assert_array_equal(c2, codes)
+    np.testing.assert_array_equal(e2, e + 5)
+    # zero block, ragged last block
+    z, ez = F8.mx_quantize(np.zeros((2, 40)), axis=1)
+    assert (z == 0).all() and (ez == -127).all()
+    c3, e3 = F8.mx_quantize(x[:, :70], axis=1)
+    assert e3.shape == (5, 70) and (e3[:, 64:] == F8.block_exponent(np.abs(x[:, 64:70]).max(1))[:, None]).all()
+
+
+def test_fp8_attention_exact_on_representable_inputs():
+    # values already E4M3 with every block maximum in [128, 256): quantisation is the identity
+    rng = np.random.default_rng(22)
+    vals = F8.e4m3_values()
+    pick = vals[(np.abs(vals) >= 1) & (np.abs(vals) < 256)]
+    def draw(shape):
+        a = rng.choice(pick, size=shape) / 64.0
+        return a
+    q, k, v = draw((40, 2, 64)), draw((70, 2, 64)), draw((70, 2, 64))
+    q8, k8, v8 = F8.quantize_qkv(q, k, v)
+    np.testing.assert_array_equal(q8, q)
+    np.testing.assert_array_equal(k8, k)
+    np.testing.assert_array_equal(v8, v)
+    o, _ = F8.fp8_attention(q, k, v)
+    np.testing.assert_allclose(o, O.attention(q, k, v), rtol=1e-12, atol=1e-12)
+
+
+def test_fp8_weight_quantisation_within_bound():
+    rng = np.random.default_rng(23)
+    for scale in (1.0, 3.0):       # flat and peaked softmax
+        q = rng.standard_normal((50, 2, 64)) * scale
+        k = rng.standard_normal((130, 2, 64))
+        v = rng.standard_normal((130, 2, 64))
+        o, bound = F8.fp8_attention(q, k, v)
+        oq = F8.fp8_attention_quantized_weights(q, k, v)
+        assert np.all(np.abs(oq - o) <= bound)
+        assert np.abs(oq - o).max() > 1e-4      # the weights really were quantised
+        # the quantised operands move the result by a few percent of its RMS, no more
+        ref = O.attention(q, k, v)
+        rel = np.sqrt(np.mean((o - ref) ** 2) / np.mean(ref ** 2))
+        assert 1e-3 < rel < 0.1
