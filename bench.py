@@ -21,7 +21,11 @@ that summary was made from the current attention sources, else null.
 sparsity RHO (the fidelity knob; every 256-query tile keeps
 ceil((1 - RHO) 512) of the 512 key tiles of 64): the step then also runs the
 block selection, and the roofline counts the attention kernel's kept keys,
-4 L_q (n_keep 64) D flops per launch."""
+4 L_q (n_keep 64) D flops per launch.
+
+--quant fp8 runs the self-attention of every stream in FP8 (the quantisation
+knob): the timed kernel is the FP8 attention, priced against the 5.0 PFLOP/s
+dense fp8 peak; its quantisation pre-pass is in `value` only."""
 from __future__ import annotations
 
 import argparse
@@ -35,6 +39,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0       # MI355X dense fp8 MFMA
 LAYERS = 30
 TIMESTEPS = (1000.0, 750.0, 500.0, 250.0)
 
@@ -52,6 +57,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--sparsity", type=float, default=0.0, metavar="RHO",
                    help="attention sparsity rho of every stream (0: dense)")
+    p.add_argument("--quant", choices=("bf16", "fp8"), default="bf16",
+                   help="self-attention precision of every stream (the quantisation knob)")
     p.add_argument("--workload", choices=("block13b", "ragged"), default="block13b",
                    help="ragged: the 8-stream batch of 1.3B-class blocks (profiling of the "
                         "elementwise kernels at 37440 rows); default 30 layers -> 4 there")
@@ -107,7 +114,8 @@ class Model:
     """Weights, pages and text K/V of every layer for a batch of streams (one
     chunk each, stream b over cache_lens[b] cached tokens), drawn on the device."""
 
-    def __init__(self, A, sh, n_layers, cache_lens, ctx_len, dev, rho=0.0, timesteps=None):
+    def __init__(self, A, sh, n_layers, cache_lens, ctx_len, dev, rho=0.0, timesteps=None,
+                 fp8=False):
         import torch
         self.A, self.sh, self.n_layers = A, sh, n_layers
         D, F, H, d = sh.dim, sh.ffn_dim, sh.n_heads, sh.head_dim
@@ -121,8 +129,9 @@ class Model:
         self.dims = A.dims_from_shape(sh)
         self.rho = rho
         self.timesteps = timesteps
+        self.fp8 = fp8
         self.batch = A.Batch([sh.chunk_tokens] * B, cache_lens, [c // T for c in cache_lens],
-                             [ctx_len] * B, sparsity=[rho] * B)
+                             [ctx_len] * B, sparsity=[rho] * B, quant=[1 if fp8 else 0] * B)
         self.ws_bytes = A.ardit_workspace_size(self.dims, self.batch)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
         from workloads.gen import block_weight_shapes, GAIN_NAMES
@@ -209,12 +218,14 @@ def cpu_baseline(model):
     m_t = O.time_modulation(TIMESTEPS[0], tw, sh.dim)
     kc, vc = O.context_kv(ctxh, w, sh.eps)
     t_ctx = time.perf_counter()
-    O.block_forward(x, ck, cv, model.cache_len // T, m_t, kc, vc, w, sh, rho=model.rho)
+    O.block_forward(x, ck, cv, model.cache_len // T, m_t, kc, vc, w, sh, rho=model.rho,
+                    fp8=model.fp8)
     t1 = time.perf_counter()
     return {"value": round((t1 - t_ctx) * 1e3, 1), "unit": "ms per chunk-denoise-step per block",
             "cores": int(threads), "kind": "oracle",
             "sample": ("one full block step (layer 0, t=1000) of the same workload: 4680 queries "
-                       f"over 32760 keys{' at sparsity %g' % model.rho if model.rho else ''}, "
+                       f"over 32760 keys{' at sparsity %g' % model.rho if model.rho else ''}"
+                       f"{' with FP8 attention' if model.fp8 else ''}, "
                        "float64 numpy; text K/V and time modulation "
                        f"({(t_ctx - t0) * 1e3:.0f} ms) excluded as on the GPU path")}
 
@@ -242,7 +253,8 @@ def main():
         args.layers = 4
     log(f"drawing {args.layers} layers on the device")
     model = Model(A, sh, args.layers, cache_lens, wl.ctx_len, dev, rho=args.sparsity,
-                  timesteps=[float(t) for t in wl.timesteps] if ragged else None)
+                  timesteps=[float(t) for t in wl.timesteps] if ragged else None,
+                  fp8=args.quant == "fp8")
     torch.cuda.synchronize()
     log("warmup")
     for k in range(args.warmup):
@@ -291,6 +303,7 @@ def main():
         workload_name = ("1.3B-class AR-DiT block: D=1536, 12x128 heads, FFN 8960, chunk 4680 "
                          "tokens (3x30x52) over a 28080-token cache, 512 text tokens, "
                          f"{args.layers} layers, t=1000/750/500/250")
+    peak = PEAK_FP8_TFLOPS if args.quant == "fp8" else PEAK_BF16_TFLOPS
     line = {
         "metric": "ms per chunk-denoise-step per block",
         "value": round(ms_block, 4),
@@ -302,18 +315,21 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if args.quant == "bf16" else "bf16 (attention fp8 e4m3)",
         "data": "synthetic (seeded normal draws, random-init weights)",
         "config": {"workload": workload_name,
                    "layers": args.layers, "chunk_tokens": L_q,
                    "kv_tokens": L_k if not ragged else [c + L_q for c in cache_lens],
                    "ctx_tokens": wl.ctx_len, "sparsity": args.sparsity,
+                   "attention_quant": args.quant,
                    "attended_keys": keys if not ragged else None},
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None if (args.sparsity or ragged) else measured_traffic(),
-                     "kernel": ("block-sparse paged self-attention" if args.sparsity
-                                else "paged self-attention"),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": (None if (args.sparsity or ragged or args.quant == "fp8")
+                                 else measured_traffic()),
+                     "kernel": (("FP8 " if args.quant == "fp8" else "")
+                                + ("block-sparse " if args.sparsity else "")
+                                + "paged self-attention"),
                      "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},
         "cpu_baseline": cpu,
     }

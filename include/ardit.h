@@ -101,7 +101,18 @@ typedef struct {
   const int32_t* ctx_lens;    /* text tokens per stream (>= 1) */
   const float* sparsity;      /* attention sparsity rho per stream in [0, 1], or NULL for all 0
                                  (block-sparse self-attention, see ardit_sparse_select) */
+  const int32_t* quant;       /* self-attention precision per stream (ardit_quant), or NULL for
+                                 all ARDIT_QUANT_BF16 */
 } ardit_batch;
+
+/* Precision of a stream's self-attention (the paper's quantisation knob Q,
+ * Section 2.1; Section 5: activations quantised online, weights never).
+ * ARDIT_QUANT_FP8 (head_dim 128 only): q, k, v and the softmax weights are
+ * OCP E4M3 with a power-of-two scale per 32 elements along each product's
+ * reduction axis (q, k: 32 dims; v, weights: 32 keys), the scale exponent
+ * floor(log2 max|x|) - 7 of the block (ardit_mx_quantize); logits, running
+ * max and denominator stay fp32.  Everything else in the block stays bf16. */
+typedef enum { ARDIT_QUANT_BF16 = 0, ARDIT_QUANT_FP8 = 1 } ardit_quant;
 
 /* Frame-paged KV cache of one layer (device memory). */
 typedef struct {
@@ -184,6 +195,15 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
  * run in this call, the lists live in the workspace). */
 int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                    const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes);
+
+/* The FP8 block quantisation the FP8 attention applies to its operands:
+ * rows of bf16 x (device, row stride ld elements, ld % 8 == 0) to E4M3 codes
+ * (device uint8 [rows][cols]) and E8M0 scales (device uint8 [rows][cols / 32]):
+ * each 32 consecutive columns take e = floor(log2 max|x|) - 7 (-127 for an
+ * all-zero block), scale byte e + 127, codes = round-to-nearest-even E4M3 of
+ * x / 2^e (|x / 2^e| < 256, no saturation).  cols % 32 == 0. */
+int ardit_mx_quantize(hipStream_t stream, const void* x, int64_t rows, int32_t cols, int32_t ld,
+                      void* codes, void* scales);
 
 /* Block selection of block-sparse self-attention (paper, Section 2.1: the
  * sparsity knob rho skips attention blocks a sparse mask leaves out; Section 5

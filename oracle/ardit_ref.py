@@ -222,7 +222,7 @@ def _after_self_attention(x, o, M, w, shape, ctx_k, ctx_v):
 
 
 def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
-                  w: dict, shape, rows=None, rho: float = 0.0, blocks=None):
+                  w: dict, shape, rows=None, rho: float = 0.0, blocks=None, fp8: bool = False):
     """One block on one chunk of one stream.
 
     x: [L_q, D] chunk activations; cache_k / cache_v: [c, H, d] the stream's
@@ -237,7 +237,8 @@ def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
 
     rho > 0 (or an explicit blocks [H, n_qblocks, n_keep] list) makes the
     self-attention block-sparse as sparse_ref defines it; the selection scores
-    the bf16-rounded rotated q and k, the values the kernels store.
+    the bf16-rounded rotated q and k, the values the kernels store.  fp8 makes
+    it the FP8 attention of fp8_ref, on the bf16-rounded q, k and v.
 
     Returns a dict with q (rotated, [L_q, H, d]), k_new, v_new ([L_q, H, d]),
     o (self-attention output, [R, D]), x1, qc, oc, x2, u, out ([R, ...])."""
@@ -248,7 +249,11 @@ def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
     K = np.concatenate([_f(cache_k), k], axis=0)
     V = np.concatenate([_f(cache_v), v], axis=0)
     sel = np.arange(x.shape[0]) if rows is None else np.asarray(rows)
-    if rho > 0.0 or blocks is not None:
+    if fp8:
+        from . import fp8_ref
+        o = fp8_ref.fp8_attention(_bf16_round(q[sel]) if rows is not None else _bf16_round(q),
+                                  _bf16_round(K), _bf16_round(V))[0].reshape(len(sel), shape.dim)
+    elif rho > 0.0 or blocks is not None:
         from . import sparse_ref
         if blocks is None:
             n_k = (K.shape[0] + sparse_ref.K_BLOCK - 1) // sparse_ref.K_BLOCK

@@ -51,7 +51,8 @@ class ardit_dims(C.Structure):
 class ardit_batch(C.Structure):
     _fields_ = [("n_streams", C.c_int32), ("q_lens", C.POINTER(C.c_int32)),
                 ("cache_lens", C.POINTER(C.c_int32)), ("frame_pos0", C.POINTER(C.c_int32)),
-                ("ctx_lens", C.POINTER(C.c_int32)), ("sparsity", C.POINTER(C.c_float))]
+                ("ctx_lens", C.POINTER(C.c_int32)), ("sparsity", C.POINTER(C.c_float)),
+                ("quant", C.POINTER(C.c_int32))]
 
 
 class ardit_kv_paged(C.Structure):
@@ -88,6 +89,7 @@ _SIGS = {
                                   _P(ardit_kv_paged), _vp]),
     "ardit_attn_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
                                  _P(ardit_kv_paged), _vp, _vp, _sz]),
+    "ardit_mx_quantize": (C.c_int, [_vp, _vp, C.c_int64, _i32, _i32, _vp, _vp]),
     "ardit_sparse_select": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
                                       _P(ardit_kv_paged), _vp, _i32, _vp, _sz]),
     "ardit_block_fwd": (C.c_int, [_vp, _P(ardit_dims), _vp, ardit_kv_paged, _i32, _i32, _vp,
@@ -168,7 +170,7 @@ class Batch:
     """Host-side batch descriptor; keeps its int32 arrays alive."""
 
     def __init__(self, q_lens=None, cache_lens=None, frame_pos0=None, ctx_lens=None,
-                 sparsity=None):
+                 sparsity=None, quant=None):
         lens = [a for a in (q_lens, cache_lens, frame_pos0, ctx_lens) if a is not None]
         n = len(lens[0]) if lens else 0
         self._arrs = []
@@ -188,7 +190,7 @@ class Batch:
             self._arrs.append(c)
             sp = C.cast(c, C.POINTER(C.c_float))
         self.struct = ardit_batch(n, arr(q_lens), arr(cache_lens), arr(frame_pos0), arr(ctx_lens),
-                                  sp)
+                                  sp, arr(quant))
         self.n = n
         self.q_lens = None if q_lens is None else [int(v) for v in q_lens]
 
@@ -236,6 +238,14 @@ def ardit_kv_append(stream, dims, batch: Batch, qkv, g_q, g_k, kv: ardit_kv_page
 def ardit_attn_fwd(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o, ws, ws_bytes):
     _check(_lib.ardit_attn_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(q),
                                C.byref(kv), _ptr(o), _ptr(ws), int(ws_bytes)), "ardit_attn_fwd")
+
+
+QUANT_BF16, QUANT_FP8 = 0, 1
+
+
+def ardit_mx_quantize(stream, x, rows, cols, ld, codes, scales):
+    _check(_lib.ardit_mx_quantize(_stream(stream), _ptr(x), int(rows), int(cols), int(ld),
+                                  _ptr(codes), _ptr(scales)), "ardit_mx_quantize")
 
 
 def ardit_sparse_select(stream, dims, batch: Batch, q, kv: ardit_kv_paged, blocks, row_stride,

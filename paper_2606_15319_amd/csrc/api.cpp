@@ -120,8 +120,26 @@ int check_batch(const ardit_dims* d, const ardit_batch* b, unsigned use) {
       if (!(r >= 0.f && r <= 1.f))
         return fail(ARDIT_EINVAL, "sparsity[%d] = %g not in [0, 1]", i, static_cast<double>(r));
     }
+  if (b->quant)
+    for (int i = 0; i < b->n_streams; ++i) {
+      if (b->quant[i] != ARDIT_QUANT_BF16 && b->quant[i] != ARDIT_QUANT_FP8)
+        return fail(ARDIT_EINVAL, "quant[%d] = %d is not a quantisation mode", i, b->quant[i]);
+      if (b->quant[i] == ARDIT_QUANT_FP8 && d->head_dim != 128)
+        return fail(ARDIT_EUNSUPPORTED, "FP8 attention needs head_dim 128 (got %d)", d->head_dim);
+    }
   return ARDIT_OK;
 }
+
+// true when some stream of the batch runs FP8 attention
+bool batch_fp8(const ardit_batch* b) {
+  if (!b->quant) return false;
+  for (int i = 0; i < b->n_streams; ++i)
+    if (b->quant[i] == ARDIT_QUANT_FP8) return true;
+  return false;
+}
+
+constexpr size_t kAlign = 256;
+size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // true when some stream of the batch runs block-sparse self-attention
 bool batch_sparse(const ardit_batch* b) {
@@ -138,9 +156,22 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // per stream.
 struct SparseBytes {
   size_t qbar = 0, scores = 0, lists = 0;
+  size_t f8q = 0, f8kv = 0;   // FP8: query codes + scales; key / value codes + scales
 };
 SparseBytes sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b) {
   SparseBytes z;
+  if (batch_fp8(b) && b->q_lens && b->cache_lens) {
+    int64_t N = 0, keys = 0;
+    for (int i = 0; i < b->n_streams; ++i) {
+      N += b->q_lens[i];
+      if (b->quant[i] == ARDIT_QUANT_FP8 && b->q_lens[i] > 0)
+        keys += kAttnKTile * ceil_div(b->cache_lens[i] + b->q_lens[i], kAttnKTile);
+    }
+    const size_t qb = static_cast<size_t>(N) * d->dim;
+    z.f8q = up(qb) + up(qb / 32);
+    const size_t kb = static_cast<size_t>(d->n_heads) * keys * d->head_dim;
+    z.f8kv = 2 * (up(kb) + up(kb / 32));
+  }
   if (!batch_sparse(b) || !b->q_lens || !b->cache_lens) return z;
   for (int i = 0; i < b->n_streams; ++i) {
     const int64_t q = b->q_lens[i];
@@ -222,8 +253,6 @@ int check_block_weights(const ardit_block_weights* w, bool ctx) {
 }
 
 // ------------------------------------------------------------ workspace
-constexpr size_t kAlign = 256;
-size_t up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Ws {
   size_t tsin, te1, te2;             // fp32 time-MLP scratch
@@ -231,6 +260,7 @@ struct Ws {
   size_t ck, cv;                     // bf16 text projections
   size_t attn;                       // fp32 partial results of split attention
   size_t sp_qbar, sp_scores, sp_lists;   // block-sparse selection (last, sized by the batch)
+  size_t f8q, f8kv;                      // FP8 attention operands
   size_t total;
 };
 
@@ -260,6 +290,8 @@ Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc,
   w.sp_qbar = take(sp.qbar);
   w.sp_scores = take(sp.scores);
   w.sp_lists = take(sp.lists);
+  w.f8q = take(sp.f8q);
+  w.f8kv = take(sp.f8kv);
   w.total = off;
   return w;
 }
@@ -416,6 +448,79 @@ AttnArgs self_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q
   return a;
 }
 
+// The streams of a planned batch whose quantisation mode is `mode`, renumbered.
+AttnArgs stream_subset(const AttnArgs& all, const ardit_batch* b, int mode, bool sparse) {
+  AttnArgs a = all;
+  int n = 0;
+  for (int i = 0; i < all.n_streams; ++i) {
+    const int m = b->quant ? b->quant[all.s[i].stream] : ARDIT_QUANT_BF16;
+    if (m == mode) a.s[n++] = all.s[i];
+  }
+  a.n_streams = n;
+  finish_plan(a, sparse);
+  return a;
+}
+
+// Self-attention of a batch: block selection first when a stream is sparse,
+// then the 16-bit streams on the bf16 kernels and the FP8 streams through the
+// quantisation pre-pass and the FP8 kernel.
+int self_attention(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const void* q,
+                   const ardit_kv_paged* kv, void* o, void* ws, const Ws& L) {
+  const int hd = d->head_dim;
+  if (!batch_fp8(b)) return run_self_attention(st, self_attn_args(d, b, q, kv, o, ws, L), hd);
+  const bool sparse = batch_sparse(b);
+  AttnArgs all = self_attn_base(d, b, q, kv, o);
+  if (sparse) {
+    plan_sparse_attention(all, b->sparsity, at<int32_t>(ws, L.sp_lists), 0,
+                          at<float>(ws, L.sp_qbar), at<float>(ws, L.sp_scores));
+    ARDIT_HIP(launch_sparse_select(st, all, hd), "block selection launch");
+  } else {
+    for (int i = 0; i < all.n_streams; ++i) {
+      AttnStream& s = all.s[i];
+      s.n_qtiles = static_cast<int32_t>(ceil_div(s.q_len, kAttnQTile));
+      s.n_tiles = static_cast<int32_t>(ceil_div(s.kv_len, kAttnKTile));
+      s.n_keep = s.n_tiles;
+    }
+  }
+  AttnArgs a16 = stream_subset(all, b, ARDIT_QUANT_BF16, sparse);
+  if (a16.total_items > 0) {
+    if (sparse) {
+      ARDIT_HIP(launch_sparse_attention(st, a16, hd), "block-sparse attention launch");
+    } else {
+      plan_attention(a16, hd, at<float>(ws, L.attn));
+      ARDIT_HIP(launch_attention(st, a16, hd, true), "self-attention launch");
+    }
+  }
+  AttnArgs a8 = stream_subset(all, b, ARDIT_QUANT_FP8, sparse);
+  if (a8.total_items > 0) {
+    uint8_t* f8q = at<uint8_t>(ws, L.f8q);
+    const size_t qb = static_cast<size_t>(sum_q(b)) * d->dim;
+    a8.q8 = f8q;
+    a8.q8s = f8q + up(qb);
+    plan_fp8_buffers(a8, hd, at<uint8_t>(ws, L.f8kv));
+    ARDIT_HIP(launch_mx_quantize_rows(st, static_cast<const bf16_t*>(q), sum_q(b), d->dim, d->dim,
+                                      a8.q8, a8.q8s), "FP8 query quantisation");
+    ARDIT_HIP(launch_fp8_kv_prep(st, a8, hd), "FP8 key / value quantisation");
+    Timing& tm = timing();
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    {
+      std::lock_guard<std::mutex> g(tm.mu);
+      if (tm.enabled) {
+        e0 = take_event(tm);
+        e1 = take_event(tm);
+      }
+    }
+    if (e0 && e1) ARDIT_HIP(hipEventRecord(e0, st), "hipEventRecord");
+    ARDIT_HIP(launch_attention_fp8(st, a8, hd, sparse), "FP8 attention launch");
+    if (e0 && e1) {
+      ARDIT_HIP(hipEventRecord(e1, st), "hipEventRecord");
+      std::lock_guard<std::mutex> g(tm.mu);
+      tm.rec.emplace_back(e0, e1);
+    }
+  }
+  return ARDIT_OK;
+}
+
 AttnArgs cross_attn_args(const ardit_dims* d, const ardit_batch* b, const void* q,
                          const void* ctx_k, const void* ctx_v, void* o, float* split_ws) {
   AttnArgs a;
@@ -484,8 +589,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
                                kv->page_table, kv->max_frames, kv->n_pages, rs),
             "v_append");
   // self-attention over [cache | chunk]
-  const AttnArgs sa = self_attn_args(d, b, q, kv, o, ws, L);
-  ARDIT_TRY(run_self_attention(st, sa, hd));
+  ARDIT_TRY(self_attention(st, d, b, q, kv, o, ws, L));
   // x1 = x + gate1 * (o W_o^T + b_o)
   e = GemmEpiArgs();
   e.bias = B16(w->b_o);
@@ -569,7 +673,7 @@ const char* ardit_status_str(int s) {
 
 const char* ardit_last_error(void) { return g_last_error.c_str(); }
 
-int ardit_version(void) { return 300; }
+int ardit_version(void) { return 400; }
 
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) {
   ARDIT_TRY(check_dims(dims));
@@ -689,8 +793,21 @@ int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch
   ARDIT_TRY(check_ptr(o, "o"));
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
-  const AttnArgs a = self_attn_args(dims, batch, q, kv, o, ws, L);
-  return run_self_attention(stream, a, dims->head_dim);
+  return self_attention(stream, dims, batch, q, kv, o, ws, L);
+}
+
+int ardit_mx_quantize(hipStream_t stream, const void* x, int64_t rows, int32_t cols, int32_t ld,
+                      void* codes, void* scales) {
+  if (!x || !codes || !scales) return fail(ARDIT_EINVAL, "pointers must be non-NULL");
+  if (rows < 0 || cols <= 0 || cols % 32 != 0)
+    return fail(ARDIT_ESHAPE, "cols %d must be a positive multiple of 32", cols);
+  if (ld < cols || ld % 8 != 0) return fail(ARDIT_ESHAPE, "ld %d must be >= cols and a multiple of 8", ld);
+  if (misaligned(x) || reinterpret_cast<uintptr_t>(codes) % 8 != 0)
+    return fail(ARDIT_EINVAL, "x must be 16-byte and codes 8-byte aligned");
+  ARDIT_HIP(launch_mx_quantize_rows(stream, static_cast<const bf16_t*>(x), rows, cols, ld,
+                                    static_cast<uint8_t*>(codes), static_cast<uint8_t*>(scales)),
+            "mx quantisation launch");
+  return ARDIT_OK;
 }
 
 int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
@@ -751,6 +868,7 @@ int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x, a
   b.frame_pos0 = &frame_pos0;
   b.ctx_lens = &ctx_len;
   b.sparsity = nullptr;
+  b.quant = nullptr;
   return ardit_block_fwd_varlen(stream, dims, &b, x, &kv, mod, ctx_k, ctx_v, w, out, ws,
                                 ws_bytes);
 }

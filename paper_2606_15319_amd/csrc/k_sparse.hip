@@ -298,29 +298,17 @@ int sparse_keep_count(int n_tiles, float rho) {
   return keep >= n_tiles ? n_tiles : static_cast<int>(keep);
 }
 
-void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32_t blk_ld,
-                           float* qbar, float* scores) {
-  // per stream in batch order: tiles, kept tiles, offset of its lists
+void finish_plan(AttnArgs& a, bool sparse) {
   AttnStream tmp[kMaxStreams];
   int n = 0;
-  int64_t packed = 0, rows = 0;
-  for (int i = 0; i < a.n_streams; ++i) {
-    AttnStream s = a.s[i];
-    s.n_qtiles = (s.q_len + kAttnQTile - 1) / kAttnQTile;
-    s.n_tiles = (s.kv_len + kAttnKTile - 1) / kAttnKTile;
-    s.n_keep = sparse_keep_count(s.n_tiles, rho ? rho[i] : 0.f);
-    s.blk_off = static_cast<int32_t>(blk_ld ? rows * blk_ld : packed);
-    s.main_tiles = s.n_tiles;
-    s.tail_begin = 0;
-    rows += static_cast<int64_t>(a.H) * s.n_qtiles;
-    packed += static_cast<int64_t>(a.H) * s.n_qtiles * s.n_keep;
-    if (s.q_len > 0) tmp[n++] = s;
-  }
+  for (int i = 0; i < a.n_streams; ++i)
+    if (a.s[i].q_len > 0) tmp[n++] = a.s[i];
   // longest items first
+  auto cost = [&](const AttnStream& x) { return sparse ? x.n_keep : x.n_tiles; };
   for (int i = 1; i < n; ++i) {
     AttnStream x = tmp[i];
     int j = i - 1;
-    while (j >= 0 && tmp[j].n_keep < x.n_keep) {
+    while (j >= 0 && cost(tmp[j]) < cost(x)) {
       tmp[j + 1] = tmp[j];
       --j;
     }
@@ -329,17 +317,35 @@ void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32
   int items = 0;
   for (int i = 0; i < n; ++i) {
     tmp[i].item_begin = items;
+    tmp[i].main_tiles = tmp[i].n_tiles;
+    tmp[i].tail_begin = 0;
     items += tmp[i].n_qtiles * a.H;
     a.s[i] = tmp[i];
   }
   a.n_streams = n;
   a.total_items = items;
-  balance_items_over_xcds(a, true);
   a.split_blocks = 0;
   a.total_tiles = 0;
   a.split_tiles = 0;
   a.part_o = nullptr;
   a.part_ml = nullptr;
+  balance_items_over_xcds(a, sparse);
+}
+
+void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32_t blk_ld,
+                           float* qbar, float* scores) {
+  // per stream in batch order: tiles, kept tiles, offset of its lists
+  int64_t packed = 0, rows = 0;
+  for (int i = 0; i < a.n_streams; ++i) {
+    AttnStream& s = a.s[i];
+    s.n_qtiles = (s.q_len + kAttnQTile - 1) / kAttnQTile;
+    s.n_tiles = (s.kv_len + kAttnKTile - 1) / kAttnKTile;
+    s.n_keep = sparse_keep_count(s.n_tiles, rho ? rho[i] : 0.f);
+    s.blk_off = static_cast<int32_t>(blk_ld ? rows * blk_ld : packed);
+    rows += static_cast<int64_t>(a.H) * s.n_qtiles;
+    packed += static_cast<int64_t>(a.H) * s.n_qtiles * s.n_keep;
+  }
+  finish_plan(a, true);
   a.blocks = blocks;
   a.blk_ld = blk_ld;
   a.qbar = qbar;

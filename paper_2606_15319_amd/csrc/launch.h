@@ -88,6 +88,12 @@ struct AttnArgs {
   int32_t* blocks;       // block-sparse: kept tiles of item (h, qt) of stream S at
                          // blocks + S.blk_off + (h n_qtiles + qt) * ld, ascending
   int32_t blk_ld;        // row stride of those lists; 0: the stream's n_keep
+  uint8_t* q8;           // FP8: E4M3 queries [rows][D] and their E8M0 scales [rows][D / 32]
+  uint8_t* q8s;
+  uint8_t* k8;           // FP8: per stream (base_off = first key) and head, keys [pad][d]
+  uint8_t* k8s;          //      with scales [pad][d / 32], values [d][pad] with scales
+  uint8_t* v8;           //      [pad / 32][d]; pad = 64 n_tiles, keys past kv_len zero
+  uint8_t* v8s;
   float* qbar;           // block-sparse: fp32 mean query of every item
   float* scores;         // block-sparse: fp32 scores, n_tiles per item, streams in plan order
   AttnStream s[kMaxStreams];
@@ -107,6 +113,21 @@ size_t attention_split_bytes(int head_dim);
 void plan_attention(AttnArgs& a, int head_dim, float* split_ws);
 hipError_t launch_attention(hipStream_t st, const AttnArgs& a, int head_dim, bool paged);
 
+// ---------------------------------------------------------- FP8 attention
+// E4M3 codes and E8M0 scales of rows of bf16: each 32 consecutive columns
+// share 2^e, e = floor(log2 max|x|) - 7; codes[r][c] = E4M3(x / 2^e), scales
+// [r][c / 32] = e + 127.  cols % 32 == 0, ld % 8 == 0.
+hipError_t launch_mx_quantize_rows(hipStream_t st, const bf16_t* x, int64_t rows, int cols, int ld,
+                                   uint8_t* codes, uint8_t* scales);
+// Sets base_off of the planned streams to their first key in the FP8 key and
+// value buffers (64 n_tiles keys each, in the plan's order) and returns the
+// bytes of k8, k8s, v8, v8s together (each part 256-byte aligned).
+size_t plan_fp8_buffers(AttnArgs& a, int head_dim, uint8_t* base);
+// Quantises the keys and values of the planned streams from the pages.
+hipError_t launch_fp8_kv_prep(hipStream_t st, const AttnArgs& a, int head_dim);
+// FP8 attention of the planned items (lists: the block-sparse lists apply).
+hipError_t launch_attention_fp8(hipStream_t st, const AttnArgs& a, int head_dim, bool lists);
+
 // ------------------------------------------------- block-sparse attention
 // Key tiles kept per query tile at sparsity rho: ceil((1 - rho) n - 1e-3) in [1, n].
 int sparse_keep_count(int n_tiles, float rho);
@@ -117,6 +138,10 @@ int sparse_keep_count(int n_tiles, float rho);
 // [items][n_tiles of the item's stream] fp32 scratch.
 void plan_sparse_attention(AttnArgs& a, const float* rho, int32_t* blocks, int32_t blk_ld,
                            float* qbar, float* scores);
+// Numbers the items of the streams in a.s (n_qtiles, n_tiles and, when
+// sparse, n_keep set): drops empty streams, orders them by decreasing cost
+// (n_keep when sparse, else n_tiles), one workgroup per item, XCDs balanced.
+void finish_plan(AttnArgs& a, bool sparse);
 // Selection: per item the scores mean(q) . mean(k) of its key tiles and its
 // n_keep best tiles, written ascending (padded with -1 up to blk_ld).
 hipError_t launch_sparse_select(hipStream_t st, const AttnArgs& a, int head_dim);

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     for code, name in A.STATUS.items():
         assert A.ardit_status_str(code) == name
     assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
-    assert A.ardit_version() == 300
+    assert A.ardit_version() == 400
 
 
 def _dims(**kw):
@@ -222,3 +222,25 @@ def test_sparse_select_validation():
                    need - 1) == -4
     assert _status(A.ardit_sparse_select, FAKE, d, b, FAKE, _kv(max_frames=4), FAKE, 6, FAKE,
                    need) == -3
+
+
+def test_quant_validation():
+    d = _dims()   # head_dim 64
+    assert _status(A.ardit_workspace_size, d, A.Batch([100], [64], quant=[2])) == -1
+    assert "quant" in A.ardit_last_error()
+    # FP8 attention is built for head_dim 128
+    assert _status(A.ardit_workspace_size, d, A.Batch([100], [64], quant=[1])) == -5
+    d128 = _dims(dim=512, n_heads=4, head_dim=128)
+    dense = A.ardit_workspace_size(d128, A.Batch([100], [64]))
+    f8 = A.ardit_workspace_size(d128, A.Batch([100], [64], quant=[1]))
+    up = lambda n: (n + 255) // 256 * 256
+    # query codes + scales for every row, keys and values of the FP8 stream padded to 64-key tiles
+    keys = 192
+    want = dense + up(100 * 512) + up(100 * 512 // 32) + 2 * (up(4 * keys * 128) + up(4 * keys * 128 // 32))
+    assert f8 == want
+
+
+def test_mx_quantize_validation():
+    assert _status(A.ardit_mx_quantize, FAKE, FAKE, 4, 48, 48, FAKE, FAKE) == -2
+    assert _status(A.ardit_mx_quantize, FAKE, FAKE, 4, 64, 60, FAKE, FAKE) == -2
+    assert _status(A.ardit_mx_quantize, FAKE, 0, 4, 64, 64, FAKE, FAKE) == -1

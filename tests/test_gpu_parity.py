@@ -609,3 +609,168 @@ def test_sparse_long_cache_more_than_1024_tiles(A):
         parity(og[off:off + n][sel], ref, f"long sparse attn stream {b}", quantum=ref)
         off += n
         r0 += H * nq
+
+
+# ---------------------------------------------------------- FP8 attention
+F8 = O.fp8_ref
+
+
+def test_mx_quantize_bit_exact(A):
+    """E4M3 codes and E8M0 scales of the block quantisation equal the oracle's
+    on rows spanning magnitudes 2^-30 .. 2^30, with zero and single-element
+    blocks."""
+    import torch
+    rng = make_rng(70)
+    rows, cols = 64, 384
+    x = rng.standard_normal((rows, cols)).astype(np.float32)
+    x *= np.exp2(rng.integers(-30, 30, size=(rows, 1))).astype(np.float32)
+    x[3, 32:64] = 0.0                     # an all-zero block
+    x[5, 64:96] = 0.0
+    x[5, 70] = -3.0e-3                    # a block with one non-zero element
+    x = bf16_round(x)
+    xd = dev_bf16(x)
+    codes = torch.empty((rows, cols), dtype=torch.uint8, device="cuda")
+    scales = torch.empty((rows, cols // 32), dtype=torch.uint8, device="cuda")
+    A.ardit_mx_quantize(None, xd, rows, cols, cols, codes, scales)
+    _sync()
+    ref_codes, ref_e = F8.mx_quantize(x, axis=1)
+    table = np.zeros(256)                  # E4M3 decode (codes 0x7f / 0xff are NaN)
+    for code in range(256):
+        sign = -1.0 if code & 0x80 else 1.0
+        ex, m = (code >> 3) & 0xF, code & 7
+        mag = m / 8 * 2.0 ** -6 if ex == 0 else (1 + m / 8) * 2.0 ** (ex - 7)
+        table[code] = np.nan if code & 0x7F == 0x7F else sign * mag
+    got = table[codes.cpu().numpy()]
+    np.testing.assert_array_equal(np.where(got == 0, 0.0, got), np.where(ref_codes == 0, 0.0, ref_codes))
+    np.testing.assert_array_equal(scales.cpu().numpy().astype(np.int64), ref_e[:, ::32] + 127)
+
+
+def _fp8_check(og, qs, ks, vs, tag, mask=None, rows=None):
+    q_in = qs if rows is None else qs[rows]
+    if mask is not None and rows is not None:
+        mask = mask[:, rows]
+    o_ref, bound = F8.fp8_attention(qs, ks, vs, mask=mask) if rows is None else \
+        _fp8_rows(qs, ks, vs, rows, mask)
+    n = len(q_in)
+    o_ref = o_ref.reshape(n, -1)
+    bound = bound.reshape(n, -1)
+    err = np.abs(og - o_ref)
+    lim = bound + half_ulp(o_ref) + 1e-6
+    assert np.all(err <= lim), f"{tag}: max err/bound {float((err / lim).max()):.3f}"
+    return float((err / lim).max())
+
+
+def _fp8_rows(qs, ks, vs, rows, mask):
+    """fp8_attention of some query rows: the query blocks quantise per row, so a
+    row subset is exact."""
+    return F8.fp8_attention(qs[rows], ks, vs, mask=mask)
+
+
+def half_ulp(ref):
+    from harness import half_ulp_bf16
+    return half_ulp_bf16(ref)
+
+
+def test_fp8_attention_mixed_batch(A):
+    """Four streams, FP8 / bf16 / FP8 / FP8, ragged query and key tiles, pages
+    shuffled and NaN-filled outside the streams: FP8 outputs within the
+    oracle's weight-quantisation bound of FP8 attention on the same bf16
+    inputs, the bf16 stream at the bf16 bar."""
+    sh = BlockShape(dim=512, n_heads=4, head_dim=128, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    q_lens, caches, quant = [600, 256, 300, 70], [1280, 0, 640, 192], [1, 0, 1, 1]
+    pc, dims, _, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 71)
+    batch = A.Batch(q_lens, caches, quant=quant)
+    _attn(A, dims, batch, q, pc.kv(A), o)
+    _sync()
+    og = host_f32(o)
+    off = 0
+    worst = 0.0
+    for b, n in enumerate(q_lens):
+        if quant[b]:
+            worst = max(worst, _fp8_check(og[off:off + n].reshape(n, -1), qs[b], ks[b], vs[b],
+                                          f"fp8 stream {b}"))
+            exact = O.attention(qs[b], ks[b], vs[b]).reshape(n, -1)
+            rel = np.sqrt(np.mean((og[off:off + n] - exact) ** 2) / np.mean(exact ** 2))
+            assert 1e-3 < rel < 0.1, rel     # quantised, and by a few percent only
+        else:
+            ref = O.attention(qs[b], ks[b], vs[b]).reshape(n, -1)
+            parity(og[off:off + n], ref, f"bf16 stream {b}", quantum=ref)
+        off += n
+    print(f"fp8 worst err / bound {worst:.3f}")
+
+
+def test_fp8_block_sparse(A):
+    """FP8 together with block-sparse attention (rho 0.8 and 0.6): the kept
+    tiles of the lists, FP8 arithmetic on them."""
+    sh = BlockShape(dim=512, n_heads=4, head_dim=128, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    q_lens, caches, rho, quant = [600, 300], [1280, 640], [0.8, 0.6], [1, 1]
+    pc, dims, _, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 72)
+    batch = A.Batch(q_lens, caches, sparsity=rho, quant=quant)
+    H = sh.n_heads
+    rows = _sparse_rows(A, dims, batch, q, pc.kv(A), row_stride=16)
+    _attn(A, dims, batch, q, pc.kv(A), o)
+    _sync()
+    og = host_f32(o)
+    off = r0 = 0
+    for b, n in enumerate(q_lens):
+        nq = (n + 255) // 256
+        lists = _check_selection(rows[r0:r0 + H * nq], qs[b], ks[b], rho[b], H, f"stream {b}")
+        mask = np.stack([S.block_mask(lists[h], n, ks[b].shape[0]) for h in range(H)])
+        _fp8_check(og[off:off + n].reshape(n, -1), qs[b], ks[b], vs[b], f"fp8 sparse {b}", mask=mask)
+        off += n
+        r0 += H * nq
+
+
+def test_fp8_attention_4680x14040(A):
+    """The 4680 x 14040 attention workload (12 heads of 128, QK-RMSNorm) in
+    FP8, sampled rows within the bound."""
+    import torch
+    wl = WORKLOADS["attn"]
+    sh = wl.shape
+    rng = make_rng(wl.wid)
+    L, c = sh.chunk_tokens, 2 * sh.chunk_tokens
+    H, d, D = sh.n_heads, sh.head_dim, sh.dim
+    q = bf16_round(O.rms_norm(rng.standard_normal((L, D), dtype=np.float32), sh.eps))
+    k = bf16_round(O.rms_norm(rng.standard_normal((c + L, D), dtype=np.float32), sh.eps))
+    v = normal_bf16(rng, (c + L, H, d))
+    T = sh.tokens_per_frame
+    pc = PagedCache(sh, [list(range((c + L) // T))], (c + L) // T)
+    pc.fill_stream(0, k.reshape(-1, H, d), v)
+    pc.upload()
+    qd = dev_bf16(q)
+    o = torch.empty_like(qd)
+    _attn(A, A.dims_from_shape(sh), A.Batch([L], [c], quant=[1]), qd, pc.kv(A), o)
+    _sync()
+    sel = sample_rows(L, seed=4)
+    _fp8_check(host_f32(o)[sel], q.reshape(L, H, d), k.reshape(-1, H, d), v, "fp8 4680x14040",
+               rows=sel)
+
+
+def test_fp8_block_varlen(A):
+    """The 1.3B-class block shape (12 heads of 128) with two streams, FP8 and
+    bf16 attention, through the block call: the FP8 stream's output against the
+    oracle's block with FP8 attention (the two sides quantise slightly
+    different bf16 roundings of q and k, so the bar is the block bar at 3x the
+    max-error tolerance), the bf16 stream at the block bar."""
+    from workloads.gen import Workload
+    sh = BlockShape(dim=1536, n_heads=12, head_dim=128, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    wl = Workload(12, "fp8_block", sh, cache_chunks=(2, 1), frame_pos0=(6, 3), ctx_len=32,
+                  timesteps=(750, 500))
+    run = BlockRun(wl, A)
+    c = run.case
+    import torch
+    run.batch = A.Batch([sh.chunk_tokens] * 2, c.cache_len, c.frame_pos0,
+                        [a.shape[0] for a in c.ctx], quant=[1, 0])
+    run.ws_bytes = A.ardit_workspace_size(run.dims, run.batch)
+    run.ws = torch.empty(run.ws_bytes, dtype=torch.uint8, device="cuda")
+    run.run()
+    _sync()
+    L = sh.chunk_tokens
+    out = host_f32(run.out)
+    for b, fp8 in enumerate((True, False)):
+        m_t = O.time_modulation(c.t[b], c.time_w, sh.dim)
+        kc, vc = O.context_kv(c.ctx[b], c.block_w, sh.eps)
+        ref = O.block_forward(c.x[b], c.cache_k[b], c.cache_v[b], c.frame_pos0[b], m_t, kc, vc,
+                              c.block_w, sh, fp8=fp8)
+        parity(out[b * L:(b + 1) * L], ref["out"], f"{'fp8' if fp8 else 'bf16'} block out {b}",
+               tol=6e-2 if fp8 else 2e-2)
