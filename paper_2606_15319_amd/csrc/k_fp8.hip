@@ -37,6 +37,7 @@ namespace ardit {
 namespace {
 
 typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int F8_BQ = 256;     // queries per item
 constexpr int F8_BKV = 64;     // keys per tile
@@ -60,6 +61,12 @@ __device__ __forceinline__ int mx_exponent(float amax) {
 // 2^-e as a float (e <= 120 for any finite fp32 block maximum, so 127 - e >= 7)
 __device__ __forceinline__ float mx_inv_scale(int e) {
   return __uint_as_float(static_cast<uint32_t>(127 - e) << 23);
+}
+
+// max of x over lanes l and l ^ 32 (one swap of the wave's halves, no LDS)
+__device__ __forceinline__ float half_pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // four floats (|x| < 256) -> four E4M3 bytes, first value in the low byte
@@ -294,26 +301,46 @@ __global__ __launch_bounds__(F8_NTHR, 1) void attn_fp8_kernel(const AttnArgs a) 
   // one 64-key tile from LDS buffer buf: scores, online softmax, P in E4M3, PV
   auto tile_step = [&](const int t, const int buf) {
     // ---- S^T = K Q^T: two 32-key blocks, two 64-dim steps
+    // all K fragments read first (two 16-byte halves each), then the four MFMAs
+    i32x8 kf[2][2];
+    uint32_t ksc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int R = 32 * kb + n;
+      ksc[kb] = sKs[buf][R];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int c0 = 4 * ks + hh, c1 = 4 * ks + 2 + hh;
+        const i32x4 a0 = *reinterpret_cast<const i32x4*>(&sK[buf][R * KROW + ((c0 ^ (R & 7)) << 4)]);
+        const i32x4 a1 = *reinterpret_cast<const i32x4*>(&sK[buf][R * KROW + ((c1 ^ (R & 7)) << 4)]);
+        kf[kb][ks] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
     f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
-      const int R = 32 * kb + n;
-      const uint32_t ksc = sKs[buf][R];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const int c0 = 4 * ks + hh, c1 = 4 * ks + 2 + hh;
-        const uint4 a0 = *reinterpret_cast<const uint4*>(&sK[buf][R * KROW + ((c0 ^ (R & 7)) << 4)]);
-        const uint4 a1 = *reinterpret_cast<const uint4*>(&sK[buf][R * KROW + ((c1 ^ (R & 7)) << 4)]);
-        const i32x8 kf = {static_cast<int>(a0.x), static_cast<int>(a0.y), static_cast<int>(a0.z),
-                          static_cast<int>(a0.w), static_cast<int>(a1.x), static_cast<int>(a1.y),
-                          static_cast<int>(a1.z), static_cast<int>(a1.w)};
-        const int sa = static_cast<int>((ksc >> (8 * (2 * ks + hh))) & 0xffu);
-        s[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf, qf[ks], s[kb], 0, 0, 0, sa, 0,
-                                                                qsc[ks]);
+        const int sa = static_cast<int>((ksc[kb] >> (8 * (2 * ks + hh))) & 0xffu);
+        s[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf[kb][ks], qf[ks], s[kb], 0, 0, 0, sa,
+                                                                0, qsc[ks]);
       }
     }
+    // V fragments for the PV product, read now so the softmax hides their latency
+    i32x8 vf[4];
+    int vsc[4];
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      const int R = 32 * db + n;
+      const int c0 = hh, c1 = 2 + hh;
+      const i32x4 v0 = *reinterpret_cast<const i32x4*>(&sV[buf][R * VROW + ((c0 ^ ((R >> 1) & 3)) << 4)]);
+      const i32x4 v1 = *reinterpret_cast<const i32x4*>(&sV[buf][R * VROW + ((c1 ^ ((R >> 1) & 3)) << 4)]);
+      vf[db] = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+      vsc[db] = sVs[buf][hh * F8_HD + R];
+    }
+    __builtin_amdgcn_sched_barrier(0);
     const int tile = F8_TIX(t);
     if (F8_BKV * tile + F8_BKV > kv_len) {   // keys past the end (last tile only)
 #pragma unroll
@@ -333,8 +360,8 @@ __global__ __launch_bounds__(F8_NTHR, 1) void attn_fp8_kernel(const AttnArgs a) 
       sb0 = fmaxf(sb0, s[0][i]);
       sb1 = fmaxf(sb1, s[1][i]);
     }
-    sb0 = fmaxf(sb0, __shfl_xor(sb0, 32, 64));
-    sb1 = fmaxf(sb1, __shfl_xor(sb1, 32, 64));
+    sb0 = half_pair_max(sb0);
+    sb1 = half_pair_max(sb1);
     const float mx = fmaxf(sb0, sb1) * c;
     if (__any(mx > m_run + 8.0f)) {
       const float m_new = fmaxf(m_run, mx);
@@ -371,17 +398,9 @@ __global__ __launch_bounds__(F8_NTHR, 1) void attn_fp8_kernel(const AttnArgs a) 
     const int psc = (hh ? e1 : e0) + 127;
     // ---- O^T += V^T P^T: four 32-dim blocks
 #pragma unroll
-    for (int db = 0; db < 4; ++db) {
-      const int R = 32 * db + n;
-      const int c0 = hh, c1 = 2 + hh;
-      const uint4 v0 = *reinterpret_cast<const uint4*>(&sV[buf][R * VROW + ((c0 ^ ((R >> 1) & 3)) << 4)]);
-      const uint4 v1 = *reinterpret_cast<const uint4*>(&sV[buf][R * VROW + ((c1 ^ ((R >> 1) & 3)) << 4)]);
-      const i32x8 vf = {static_cast<int>(v0.x), static_cast<int>(v0.y), static_cast<int>(v0.z),
-                        static_cast<int>(v0.w), static_cast<int>(v1.x), static_cast<int>(v1.y),
-                        static_cast<int>(v1.z), static_cast<int>(v1.w)};
-      const int vsc = sVs[buf][hh * F8_HD + R];
-      o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf, pf, o[db], 0, 0, 0, vsc, 0, psc);
-    }
+    for (int db = 0; db < 4; ++db)
+      o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[db], pf, o[db], 0, 0, 0, vsc[db], 0,
+                                                              psc);
   };
 
   // two tiles of loads in flight: register set t & 1 holds tile t until stored
@@ -409,7 +428,9 @@ __global__ __launch_bounds__(F8_NTHR, 1) void attn_fp8_kernel(const AttnArgs a) 
 #undef F8_STORE
 #undef F8_TIX
   // ---- normalised bf16 output: lane holds dims 32 db + 8 g + 4 hh + 0..3 of its query
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const auto lp = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run),
+                                                    false, false);
+  const float l_tot = __uint_as_float(lp[0]) + __uint_as_float(lp[1]);
   const float inv = 1.0f / l_tot;
   const int ql = qt * F8_BQ + wave * 32 + n;
   if (ql < S.q_len) {
