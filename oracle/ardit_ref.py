@@ -268,13 +268,14 @@ def block_forward(x, cache_k, cache_v, frame_pos0: int, m_t, ctx_k, ctx_v,
 
 
 def full_sequence_forward(xs, m_ts, frame_pos0: int, ctx_k, ctx_v, w: dict,
-                          shape, window=None):
+                          shape, window=None, sink: int = 0):
     """Block-causal full-sequence version over chunks 0..C-1 of one stream.
 
     xs: list of [L_q, D] chunks; m_ts: per-chunk [6, D] time modulation.
     Chunk c's frames start at frame_pos0 + c * frames.  Token i sees token j
-    iff chunk(j) <= chunk(i) (and chunk(i) - chunk(j) <= window when a window
-    of earlier chunks is given).  Used only to pin the chunk-with-cache form."""
+    iff chunk(j) <= chunk(i) (and, when a window of earlier chunks is given,
+    chunk(i) - chunk(j) <= window or chunk(j) < sink: the sink chunks stay
+    visible).  Used only to pin the chunk-with-cache form."""
     C = len(xs)
     Lq = shape.chunk_tokens
     x = np.concatenate([_f(a) for a in xs], axis=0)
@@ -287,7 +288,7 @@ def full_sequence_forward(xs, m_ts, frame_pos0: int, ctx_k, ctx_v, w: dict,
     q, k, v = _qkv_rope(x, Mtok, w, shape, pos)
     mask = chunk_of[None, :] <= chunk_of[:, None]
     if window is not None:
-        mask &= (chunk_of[:, None] - chunk_of[None, :]) <= window
+        mask &= ((chunk_of[:, None] - chunk_of[None, :]) <= window) | (chunk_of[None, :] < sink)
     o = attention(q, k, v, mask=mask).reshape(-1, shape.dim)
     res = _after_self_attention(x, o, Mtok, w, shape, ctx_k, ctx_v)
     res.update({"q": q, "k": k, "v": v, "o": o})

@@ -642,3 +642,93 @@ def test_fp8_weight_quantisation_within_bound():
         ref = O.attention(q, k, v)
         rel = np.sqrt(np.mean((o - ref) ** 2) / np.mean(ref ** 2))
         assert 1e-3 < rel < 0.1
+
+
+# --------------------------------------------------------------------------
+# chunk generation: sampler, commit, sink + window
+# --------------------------------------------------------------------------
+CH = O.chunk_ref
+
+
+def test_sampler_step_closed_forms():
+    rng = np.random.default_rng(31)
+    x0 = rng.standard_normal((6, 8))
+    eps = rng.standard_normal((6, 8))
+    eps2 = rng.standard_normal((6, 8))
+    for t, tn in ((1000.0, 750.0), (750.0, 500.0), (250.0, None), (500.0, 0.0)):
+        tau = t / 1000.0
+        x = (1 - tau) * x0 + tau * eps
+        v = eps - x0                       # the exact rectified-flow velocity
+        out = CH.sampler_step(x, v, t, tn, eps2)
+        if tn is None or tn == 0.0:
+            np.testing.assert_allclose(out, x0, rtol=1e-13, atol=1e-13)
+        else:
+            np.testing.assert_allclose(out, (1 - tn / 1000) * x0 + tn / 1000 * eps2, rtol=1e-13,
+                                       atol=1e-13)
+
+
+def test_window_listing_and_slots():
+    # sink 1, window 2: chunk c sees chunk 0 and the two chunks before it
+    assert [CH.window_chunks(c, 1, 2) for c in range(6)] == \
+        [[], [0], [0, 1], [0, 1, 2], [0, 2, 3], [0, 3, 4]]
+    assert [CH.window_chunks(c, 0, 1) for c in range(4)] == [[], [0], [1], [2]]
+    assert CH.window_chunks(9, 2, 3) == [0, 1, 6, 7, 8]
+    # no two chunks in the cache (nor the current one) share a physical slot
+    for sink in range(3):
+        for W in (1, 3, 7):
+            for c in range(40):
+                slots = [CH.chunk_slot(k, sink, W) for k in CH.window_chunks(c, sink, W) + [c]]
+                assert len(set(slots)) == len(slots)
+                assert max(slots) < sink + W + 1
+    # chunk 4, sink 1, window 2, 3 frames per chunk: chunks 0 (slot 0), 2 (slot 1 + 1 mod 3 = 2),
+    # 3 (slot 3), then chunk 4 itself in slot 1 + 3 mod 3 = 1
+    table, cached = CH.window_page_table(4, 1, 2, 3)
+    assert cached == 9 and table.tolist() == [0, 1, 2, 6, 7, 8, 9, 10, 11, 3, 4, 5]
+
+
+def test_sink_window_generation_equals_masked_full_sequence():
+    """Chunk by chunk with the cache evicted to sink + window equals the
+    block-causal full sequence whose mask keeps only the sink and the window."""
+    sh = TINY
+    w, tw = _tiny_weights(12)
+    rng = np.random.default_rng(12)
+    C, sink, W = 5, 1, 2
+    xs = [rng.standard_normal((sh.chunk_tokens, sh.dim)) for _ in range(C)]
+    m_ts = [O.time_modulation(t, tw, sh.dim) for t in (1000.0, 750.0, 500.0, 250.0, 1000.0)]
+    ctx = rng.standard_normal((4, sh.dim))
+    kc, vc = O.context_kv(ctx, w, sh.eps)
+    full = O.full_sequence_forward(xs, m_ts, 5, kc, vc, w, sh, window=W, sink=sink)
+    L = sh.chunk_tokens
+    keys, vals = {}, {}
+    for c in range(C):
+        held = CH.window_chunks(c, sink, W)
+        ck = np.concatenate([keys[k] for k in held]) if held else np.zeros((0, sh.n_heads, sh.head_dim))
+        cv = np.concatenate([vals[k] for k in held]) if held else np.zeros((0, sh.n_heads, sh.head_dim))
+        r = O.block_forward(xs[c], ck, cv, 5 + c * sh.frames, m_ts[c], kc, vc, w, sh)
+        np.testing.assert_allclose(r["out"], full["out"][c * L:(c + 1) * L], rtol=1e-11, atol=1e-11)
+        keys[c], vals[c] = r["k_new"], r["v_new"]
+    # chunk 4 without the sink would differ
+    nosink = O.full_sequence_forward(xs, m_ts, 5, kc, vc, w, sh, window=W, sink=0)
+    assert np.abs(nosink["out"][4 * L:] - full["out"][4 * L:]).max() > 1e-6
+
+
+def test_generate_chunk_two_steps_by_hand():
+    """generate_chunk against the steps written out: two denoising steps of a
+    one-layer stack, then the commit pass at t = 0."""
+    sh = TINY
+    w, tw = _tiny_weights(13)
+    rng = np.random.default_rng(13)
+    x_init = rng.standard_normal((sh.chunk_tokens, sh.dim))
+    eps = rng.standard_normal((sh.chunk_tokens, sh.dim))
+    ck = rng.standard_normal((8, sh.n_heads, sh.head_dim))
+    cv = rng.standard_normal((8, sh.n_heads, sh.head_dim))
+    ctx = rng.standard_normal((4, sh.dim))
+    kc, vc = O.context_kv(ctx, w, sh.eps)
+    x0, committed, xs = CH.generate_chunk(x_init, [eps], [1000.0, 500.0], [(ck, cv)], 2, tw,
+                                          [(kc, vc)], [w], sh)
+    v1 = O.block_forward(x_init, ck, cv, 2, O.time_modulation(1000.0, tw, sh.dim), kc, vc, w, sh)["out"]
+    x1 = 0.5 * (x_init - v1) + 0.5 * eps
+    v2 = O.block_forward(x1, ck, cv, 2, O.time_modulation(500.0, tw, sh.dim), kc, vc, w, sh)["out"]
+    np.testing.assert_allclose(x0, x1 - 0.5 * v2, rtol=1e-12, atol=1e-12)
+    r = O.block_forward(x0, ck, cv, 2, O.time_modulation(0.0, tw, sh.dim), kc, vc, w, sh)
+    np.testing.assert_allclose(committed[0][0], r["k_new"], rtol=1e-12, atol=1e-12)
