@@ -67,6 +67,7 @@ extern "C" {
 
 #define ARDIT_MAX_STREAMS 64
 #define ARDIT_TIME_FREQ_DIM 256
+#define ARDIT_MAX_STEPS 16     /* denoising steps of one chunk in ardit_chunk_generate */
 
 typedef enum {
   ARDIT_OK = 0,
@@ -252,6 +253,66 @@ int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batc
                     int32_t n_layers, const void* x, const ardit_kv_paged* kv, const float* mod,
                     const void* const* ctx_k, const void* const* ctx_v,
                     const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes);
+
+/* Page table of one stream under a sink + sliding-window cache (paper,
+ * Section 2.1: the cache keeps a few sink chunks plus the most recent W
+ * chunks; Sections 3.2 and 4.4: frame pages behind a logical table).  While
+ * chunk `chunk` (0-based) is generated, the stream's cache holds chunks
+ * 0 .. min(sink, chunk) - 1 and max(sink, chunk - window) .. chunk - 1, in that
+ * order.  Chunk k lives in slot k when k < sink, else in slot
+ * sink + (k - sink) mod (window + 1), so the slot of the chunk being generated
+ * never holds a chunk still in the window; slot s owns pages
+ * page_base + s * frames_per_chunk + f, f < frames_per_chunk.  A stream thus
+ * needs (sink + window + 1) * frames_per_chunk pages.  Writes the held
+ * chunks' pages followed by chunk `chunk`'s into table[0 ..
+ * (held + 1) * frames_per_chunk) (host int32, max_frames entries; the rest is
+ * untouched) and the held frame count to *cache_frames: the stream's
+ * cache_len is *cache_frames * lat_h * lat_w.  Keys keep the RoPE positions
+ * of their absolute frames, so frame_pos0 stays chunk * frames_per_chunk.
+ * Host only: makes no HIP call.  ARDIT_ECAPACITY when max_frames is too short
+ * or the pages overflow int32. */
+int ardit_window_pages(int32_t chunk, int32_t sink, int32_t window, int32_t frames_per_chunk,
+                       int32_t page_base, int32_t* table, int32_t max_frames,
+                       int32_t* cache_frames);
+
+/* One chunk of every stream of the batch, end to end (paper, Section 2.1,
+ * "AR-DiT": a chunk is denoised in S steps by the stack attending to the
+ * stream's cache, then appended to it; Appendix A: S is a fidelity knob).
+ * The paper does not give the sampler or the commit; computed here:
+ *  - step i of stream b (timestep t = t_host[b * t_ld + i] in [0, 1000], tau = t / 1000):
+ *    M = ardit_time_mod(t); v = ardit_stack_fwd(x_tau) (the velocity);
+ *    x0_hat = x_tau - tau v; the next step starts from
+ *    (1 - tau') x0_hat + tau' eps_{i+1}, tau' its timestep / 1000; the last step
+ *    keeps x0_hat (the clean chunk, written to x0_out).  The update runs in
+ *    fp32 on bf16 operands and stores bf16.
+ *  - the commit: one more pass of the stack on x0_hat at t = 0, whose keys and
+ *    values are what slots [cache_len, cache_len + L_q) of every layer's pages
+ *    hold when the call's work completes (the caller then commits the chunk
+ *    through its page table, e.g. ardit_window_pages for the next chunk).
+ * Streams run in lockstep: pass i covers the streams with n_steps[b] >= i, as
+ * step i of those with n_steps[b] > i and the commit of those with
+ * n_steps[b] == i; n_steps must be non-increasing along the batch so each pass
+ * is a prefix of it.  A pass that only commits skips the work after the last
+ * layer's key/value append (its output is not used).
+ *   n_steps: host [n_streams], each in [1, ARDIT_MAX_STEPS].
+ *   t_host:  host, row b of t_ld >= n_steps[0] entries: the stream's timesteps.
+ *   x_init:  device bf16 [sum q_lens][D], the starting noise x_{tau_0} (read only).
+ *   noise:   device bf16 [n_steps[0] - 1][sum q_lens][D]; slab i is eps_{i+1}
+ *            (rows of streams without a step i + 1 are not read); may be NULL
+ *            when n_steps[0] == 1.
+ *   kv, ctx_k, ctx_v, w: per-layer host arrays of n_layers entries, as for
+ *            ardit_stack_fwd; tw: the shared time MLP.
+ *   x0_out:  device bf16 [sum q_lens][D], the clean chunk; must not overlap
+ *            x_init, noise or the workspace.
+ *   ws:      ardit_workspace_size of this batch (it includes the modulation
+ *            and velocity buffers this call needs).
+ * batch->sparsity and batch->quant apply to every pass. */
+int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                         int32_t n_layers, const int32_t* n_steps, const float* t_host,
+                         int32_t t_ld, const void* x_init, const void* noise,
+                         const ardit_kv_paged* kv, const ardit_time_weights* tw,
+                         const void* const* ctx_k, const void* const* ctx_v,
+                         const ardit_block_weights* w, void* x0_out, void* ws, size_t ws_bytes);
 
 /* Kernel timing: while enabled, block calls record HIP events on their stream
  * around every launch of the self-attention kernel (for sparse streams the

@@ -69,14 +69,19 @@ def window_page_table(c: int, sink: int, window: int, frames: int):
     return np.array(table, dtype=np.int64), len(held) * frames
 
 
-def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv, ws: list, shape):
+def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv, ws: list, shape,
+                   store=None):
     """One chunk of one stream through an L-layer stack.
 
     x_init: [L_q, D] starting noise; noise: fresh noise of the steps after the
     first ([S - 1][L_q, D]); ts: the S timesteps; caches: per layer (k, v) of
     the held chunks ([c, H, d] each, logical order); ctx_kv: per layer (K_c,
-    V_c); ws: per-layer weights.  Returns (x0, committed per-layer (k, v) of
-    the chunk, the per-step inputs x_tau)."""
+    V_c); ws: per-layer weights.  store: optional rounding applied where an
+    implementation stores a tensor between operations (each layer's output,
+    the sampler's result, the committed keys and values); None keeps float64
+    throughout.  Returns (x0, committed per-layer (k, v) of the chunk, the
+    per-step inputs x_tau)."""
+    keep = (lambda a: a) if store is None else (lambda a: np.asarray(store(a), np.float64))
     x = np.asarray(x_init, np.float64)
     xs = []
     for s, t in enumerate(ts):
@@ -85,10 +90,10 @@ def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv,
         h = x
         for layer, w in enumerate(ws):
             ck, cv = caches[layer]
-            h = block_forward(h, ck, cv, frame_pos0, m_t, ctx_kv[layer][0], ctx_kv[layer][1], w,
-                              shape)["out"]
+            h = keep(block_forward(h, ck, cv, frame_pos0, m_t, ctx_kv[layer][0], ctx_kv[layer][1],
+                                   w, shape)["out"])
         nxt = ts[s + 1] if s + 1 < len(ts) else None
-        x = sampler_step(x, h, t, nxt, noise[s] if nxt is not None else None)
+        x = keep(sampler_step(x, h, t, nxt, noise[s] if nxt is not None else None))
     x0 = x
     m0 = time_modulation(0.0, tw, shape.dim)
     committed = []
@@ -96,6 +101,6 @@ def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv,
     for layer, w in enumerate(ws):
         ck, cv = caches[layer]
         r = block_forward(h, ck, cv, frame_pos0, m0, ctx_kv[layer][0], ctx_kv[layer][1], w, shape)
-        committed.append((r["k_new"], r["v_new"]))
-        h = r["out"]
+        committed.append((keep(r["k_new"]), keep(r["v_new"])))
+        h = keep(r["out"])
     return x0, committed, xs

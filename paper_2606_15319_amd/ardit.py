@@ -28,6 +28,7 @@ except ImportError:  # plain C-ABI use without torch
 _lib = C.CDLL(LIB_PATH)
 
 ARDIT_MAX_STREAMS = 64
+ARDIT_MAX_STEPS = 16
 STATUS = {0: "ARDIT_OK", -1: "ARDIT_EINVAL", -2: "ARDIT_ESHAPE", -3: "ARDIT_ECAPACITY",
           -4: "ARDIT_EWORKSPACE", -5: "ARDIT_EUNSUPPORTED", -6: "ARDIT_EHIP"}
 
@@ -100,6 +101,11 @@ _SIGS = {
     "ardit_stack_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _i32, _vp,
                                   _P(ardit_kv_paged), _vp, _P(_vp), _P(_vp),
                                   _P(ardit_block_weights), _vp, _vp, _sz]),
+    "ardit_window_pages": (C.c_int, [_i32, _i32, _i32, _i32, _i32, _P(_i32), _i32, _P(_i32)]),
+    "ardit_chunk_generate": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _i32, _P(_i32),
+                                       _P(C.c_float), _i32, _vp, _vp, _P(ardit_kv_paged),
+                                       _P(ardit_time_weights), _P(_vp), _P(_vp),
+                                       _P(ardit_block_weights), _vp, _vp, _sz]),
     "ardit_timing_enable": (C.c_int, [C.c_int]),
     "ardit_timing_collect": (C.c_int, [_P(_i32), _P(C.c_double)]),
 }
@@ -281,6 +287,40 @@ def ardit_stack_fwd(stream, dims, batch: Batch, x, kvs, mod, ctx_ks, ctx_vs, ws_
     _check(_lib.ardit_stack_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), L, _ptr(x),
                                 kv_arr, _ptr(mod), ck, cv, w_arr, _ptr(out), _ptr(ws),
                                 int(ws_bytes)), "ardit_stack_fwd")
+
+
+def ardit_window_pages(chunk, sink, window, frames_per_chunk, page_base=0, max_frames=None):
+    """Returns (table entries of the held chunks then the chunk, cached frames)."""
+    if max_frames is None:
+        max_frames = (int(sink) + int(window) + 1) * int(frames_per_chunk)
+    table = (C.c_int32 * max(int(max_frames), 1))()
+    cached = C.c_int32(0)
+    _check(_lib.ardit_window_pages(int(chunk), int(sink), int(window), int(frames_per_chunk),
+                                   int(page_base), table, int(max_frames), C.byref(cached)),
+           "ardit_window_pages")
+    n = cached.value + int(frames_per_chunk)
+    return [table[i] for i in range(n)], cached.value
+
+
+def ardit_chunk_generate(stream, dims, batch: Batch, n_steps, timesteps, x_init, noise, kvs,
+                         tw: ardit_time_weights, ctx_ks, ctx_vs, ws_list, x0_out, ws, ws_bytes):
+    """timesteps: per stream, the list of its n_steps[b] timesteps."""
+    L = len(kvs)
+    B = len(n_steps)
+    t_ld = max(1, max(int(s) for s in n_steps))
+    t = (C.c_float * (B * t_ld))()
+    for b, ts in enumerate(timesteps):
+        for i, v in enumerate(ts):
+            t[b * t_ld + i] = float(v)
+    ns = (C.c_int32 * B)(*[int(v) for v in n_steps])
+    kv_arr = (ardit_kv_paged * L)(*kvs)
+    w_arr = (ardit_block_weights * L)(*ws_list)
+    ck = (C.c_void_p * L)(*[_ptr(x) for x in ctx_ks])
+    cv = (C.c_void_p * L)(*[_ptr(x) for x in ctx_vs])
+    _check(_lib.ardit_chunk_generate(_stream(stream), C.byref(dims), C.byref(batch.struct), L, ns,
+                                     t, t_ld, _ptr(x_init), _ptr(noise), kv_arr, C.byref(tw), ck,
+                                     cv, w_arr, _ptr(x0_out), _ptr(ws), int(ws_bytes)),
+           "ardit_chunk_generate")
 
 
 def ardit_timing_enable(enable: bool):

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libardit.so")
-SOURCES = ["api.cpp", "k_gemm.hip", "k_attn.hip", "k_elem.hip", "k_sparse.hip", "k_fp8.hip"]
+SOURCES = ["api.cpp", "k_gemm.hip", "k_attn.hip", "k_elem.hip", "k_sparse.hip", "k_fp8.hip",
+           "k_chunk.hip"]
 
 
 def hipcc() -> str:

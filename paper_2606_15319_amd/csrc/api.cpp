@@ -261,6 +261,7 @@ struct Ws {
   size_t attn;                       // fp32 partial results of split attention
   size_t sp_qbar, sp_scores, sp_lists;   // block-sparse selection (last, sized by the batch)
   size_t f8q, f8kv;                      // FP8 attention operands
+  size_t gmod, gv;                       // chunk generation: fp32 modulation, bf16 velocity
   size_t total;
 };
 
@@ -292,6 +293,8 @@ Ws ws_layout(const ardit_dims* d, int B, int64_t N, int64_t Nc,
   w.sp_lists = take(sp.lists);
   w.f8q = take(sp.f8q);
   w.f8kv = take(sp.f8kv);
+  w.gmod = take(sizeof(float) * B * 6 * D);
+  w.gv = take(2 * N * D);
   w.total = off;
   return w;
 }
@@ -553,9 +556,12 @@ AttnArgs cross_attn_args(const ardit_dims* d, const ardit_batch* b, const void* 
 }
 
 // the block chain on validated arguments
+// (kv_only: stop once the chunk's keys and values are in the pages; out is
+// not written)
 int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const void* xin,
                 const ardit_kv_paged* kv, const float* mod, const void* ctx_k, const void* ctx_v,
-                const ardit_block_weights* w, void* out, void* ws, const Ws& L) {
+                const ardit_block_weights* w, void* out, void* ws, const Ws& L,
+                bool kv_only = false) {
   const int N = static_cast<int>(sum_q(b));
   const int D = d->dim, F = d->ffn_dim, H = d->n_heads, hd = d->head_dim;
   const int Lq = chunk_tokens(d);
@@ -588,6 +594,7 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
                                static_cast<bf16_t*>(kv->v_pages), true, tokens_per_frame(d),
                                kv->page_table, kv->max_frames, kv->n_pages, rs),
             "v_append");
+  if (kv_only) return ARDIT_OK;
   // self-attention over [cache | chunk]
   ARDIT_TRY(self_attention(st, d, b, q, kv, o, ws, L));
   // x1 = x + gate1 * (o W_o^T + b_o)
@@ -637,6 +644,37 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   return ARDIT_OK;
 }
 
+int check_time_weights(const ardit_time_weights* tw) {
+  if (!tw) return fail(ARDIT_EINVAL, "time weights NULL");
+  const void* p[] = {tw->w_t1, tw->b_t1, tw->w_t2, tw->b_t2, tw->w_m, tw->b_m};
+  const char* n[] = {"w_t1", "b_t1", "w_t2", "b_t2", "w_m", "b_m"};
+  for (int i = 0; i < 6; ++i) ARDIT_TRY(check_ptr(p[i], n[i]));
+  return ARDIT_OK;
+}
+
+// sinusoid of t, then the time MLP, into mod_out [B][6][D]
+int time_mod_chain(hipStream_t st, const ardit_dims* d, int B, const float* t_host,
+                   const ardit_time_weights* tw, float* mod_out, void* ws, const Ws& L) {
+  const int D = d->dim;
+  float* s = at<float>(ws, L.tsin);
+  float* e1 = at<float>(ws, L.te1);
+  float* e2 = at<float>(ws, L.te2);
+  auto B16 = [](const void* q) { return static_cast<const bf16_t*>(q); };
+  ARDIT_HIP(launch_time_sinusoid(st, t_host, B, s), "time sinusoid");
+  ARDIT_HIP(launch_linear_small(st, s, B, ARDIT_TIME_FREQ_DIM, B16(tw->w_t1), B16(tw->b_t1), D,
+                                e1, false), "time mlp 1");
+  ARDIT_HIP(launch_linear_small(st, e1, B, D, B16(tw->w_t2), B16(tw->b_t2), D, e2, true),
+            "time mlp 2");
+  ARDIT_HIP(launch_linear_small(st, e2, B, D, B16(tw->w_m), B16(tw->b_m), 6 * D, mod_out, true),
+            "time modulation");
+  return ARDIT_OK;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return na && nb && x < y + nb && y < x + na;
+}
+
 int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
                      const ardit_kv_paged* kv, const float* mod, const void* ctx_k,
                      const void* ctx_v, const ardit_block_weights* w, const void* out) {
@@ -673,7 +711,7 @@ const char* ardit_status_str(int s) {
 
 const char* ardit_last_error(void) { return g_last_error.c_str(); }
 
-int ardit_version(void) { return 400; }
+int ardit_version(void) { return 500; }
 
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) {
   ARDIT_TRY(check_dims(dims));
@@ -699,25 +737,12 @@ int ardit_time_mod(hipStream_t stream, const ardit_dims* dims, int32_t n_streams
   if (n_streams < 1 || n_streams > ARDIT_MAX_STREAMS)
     return fail(ARDIT_EINVAL, "n_streams %d not in [1, %d]", n_streams, ARDIT_MAX_STREAMS);
   if (!t_host) return fail(ARDIT_EINVAL, "t_host is NULL");
-  if (!tw) return fail(ARDIT_EINVAL, "time weights NULL");
-  const void* p[] = {tw->w_t1, tw->b_t1, tw->w_t2, tw->b_t2, tw->w_m, tw->b_m, mod_out, ws};
-  const char* n[] = {"w_t1", "b_t1", "w_t2", "b_t2", "w_m", "b_m", "mod_out", "ws"};
-  for (int i = 0; i < 8; ++i) ARDIT_TRY(check_ptr(p[i], n[i]));
+  ARDIT_TRY(check_time_weights(tw));
+  ARDIT_TRY(check_ptr(mod_out, "mod_out"));
+  ARDIT_TRY(check_ptr(ws, "ws"));
   const Ws L = ws_layout(dims, n_streams, 0, 0);
   if (ws_bytes < L.h) return fail(ARDIT_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.h);
-  const int D = dims->dim;
-  float* s = at<float>(ws, L.tsin);
-  float* e1 = at<float>(ws, L.te1);
-  float* e2 = at<float>(ws, L.te2);
-  auto B16 = [](const void* q) { return static_cast<const bf16_t*>(q); };
-  ARDIT_HIP(launch_time_sinusoid(stream, t_host, n_streams, s), "time sinusoid");
-  ARDIT_HIP(launch_linear_small(stream, s, n_streams, ARDIT_TIME_FREQ_DIM, B16(tw->w_t1),
-                                B16(tw->b_t1), D, e1, false), "time mlp 1");
-  ARDIT_HIP(launch_linear_small(stream, e1, n_streams, D, B16(tw->w_t2), B16(tw->b_t2), D, e2,
-                                true), "time mlp 2");
-  ARDIT_HIP(launch_linear_small(stream, e2, n_streams, D, B16(tw->w_m), B16(tw->b_m), 6 * D,
-                                mod_out, true), "time modulation");
-  return ARDIT_OK;
+  return time_mod_chain(stream, dims, n_streams, t_host, tw, mod_out, ws, L);
 }
 
 int ardit_ctx_kv(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
@@ -889,6 +914,124 @@ int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batc
   for (int l = 0; l < n_layers; ++l)
     ARDIT_TRY(block_chain(stream, dims, batch, l == 0 ? x : out, &kv[l], mod, ctx_k[l], ctx_v[l],
                           &w[l], out, ws, L));
+  return ARDIT_OK;
+}
+
+int ardit_window_pages(int32_t chunk, int32_t sink, int32_t window, int32_t frames_per_chunk,
+                       int32_t page_base, int32_t* table, int32_t max_frames,
+                       int32_t* cache_frames) {
+  if (chunk < 0 || sink < 0 || window < 0 || frames_per_chunk < 1 || page_base < 0)
+    return fail(ARDIT_EINVAL, "chunk %d, sink %d, window %d, page_base %d must be >= 0 and "
+                "frames_per_chunk %d >= 1", chunk, sink, window, page_base, frames_per_chunk);
+  if (!table || !cache_frames) return fail(ARDIT_EINVAL, "table and cache_frames must be non-NULL");
+  const int64_t slots = static_cast<int64_t>(sink) + window + 1;
+  if (page_base + slots * frames_per_chunk > INT32_MAX)
+    return fail(ARDIT_ECAPACITY, "pages of the stream's slots exceed int32");
+  // held chunks in logical order: the sink, then the last `window` before chunk
+  const int64_t n_sink = chunk < sink ? chunk : sink;
+  const int64_t w_begin = chunk - static_cast<int64_t>(window) > sink ? chunk - window : sink;
+  const int64_t held = n_sink + (chunk > w_begin ? chunk - w_begin : 0);
+  if ((held + 1) * frames_per_chunk > max_frames)
+    return fail(ARDIT_ECAPACITY, "table of %d frames holds fewer than the %lld the window needs",
+                max_frames, static_cast<long long>((held + 1) * frames_per_chunk));
+  auto slot_of = [&](int64_t k) -> int64_t {
+    return k < sink ? k : sink + (k - sink) % (static_cast<int64_t>(window) + 1);
+  };
+  int64_t f = 0;
+  auto put = [&](int64_t k) {
+    const int64_t first = page_base + slot_of(k) * frames_per_chunk;
+    for (int j = 0; j < frames_per_chunk; ++j) table[f++] = static_cast<int32_t>(first + j);
+  };
+  for (int64_t k = 0; k < n_sink; ++k) put(k);
+  for (int64_t k = w_begin; k < chunk; ++k) put(k);
+  put(chunk);
+  *cache_frames = static_cast<int32_t>(held * frames_per_chunk);
+  return ARDIT_OK;
+}
+
+int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                         int32_t n_layers, const int32_t* n_steps, const float* t_host,
+                         int32_t t_ld, const void* x_init, const void* noise,
+                         const ardit_kv_paged* kv, const ardit_time_weights* tw,
+                         const void* const* ctx_k, const void* const* ctx_v,
+                         const ardit_block_weights* w, void* x0_out, void* ws, size_t ws_bytes) {
+  ARDIT_TRY(check_dims(dims));
+  ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache | kUsePos | kUseCtx | kChunkQ));
+  if (n_layers < 1) return fail(ARDIT_EINVAL, "n_layers %d must be >= 1", n_layers);
+  if (!kv || !ctx_k || !ctx_v || !w) return fail(ARDIT_EINVAL, "per-layer arrays must be non-NULL");
+  if (!n_steps || !t_host) return fail(ARDIT_EINVAL, "n_steps and t_host must be non-NULL");
+  const int B = batch->n_streams;
+  const int S0 = n_steps[0];
+  for (int b = 0; b < B; ++b) {
+    if (n_steps[b] < 1 || n_steps[b] > ARDIT_MAX_STEPS)
+      return fail(ARDIT_EINVAL, "n_steps[%d] = %d not in [1, %d]", b, n_steps[b],
+                  ARDIT_MAX_STEPS);
+    if (b > 0 && n_steps[b] > n_steps[b - 1])
+      return fail(ARDIT_EINVAL, "n_steps must be non-increasing along the batch (stream %d)", b);
+  }
+  if (t_ld < S0) return fail(ARDIT_EINVAL, "t_ld %d below n_steps[0] = %d", t_ld, S0);
+  for (int b = 0; b < B; ++b)
+    for (int i = 0; i < n_steps[b]; ++i) {
+      const float t = t_host[static_cast<size_t>(b) * t_ld + i];
+      if (!(t >= 0.f && t <= 1000.f))
+        return fail(ARDIT_EINVAL, "timestep %g of stream %d step %d not in [0, 1000]",
+                    static_cast<double>(t), b, i);
+    }
+  ARDIT_TRY(check_time_weights(tw));
+  ARDIT_TRY(check_ptr(x_init, "x_init"));
+  ARDIT_TRY(check_ptr(x0_out, "x0_out"));
+  if (S0 > 1) ARDIT_TRY(check_ptr(noise, "noise"));
+  Ws L;
+  ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  float* mod = at<float>(ws, L.gmod);
+  bf16_t* vel = at<bf16_t>(ws, L.gv);
+  for (int l = 0; l < n_layers; ++l)
+    ARDIT_TRY(check_block_args(dims, batch, x_init, &kv[l], mod, ctx_k[l], ctx_v[l], &w[l], vel));
+  const int64_t N = sum_q(batch);
+  const int D = dims->dim;
+  const size_t xbytes = 2 * static_cast<size_t>(N) * D;
+  if (overlaps(x0_out, xbytes, x_init, xbytes) ||
+      (S0 > 1 && overlaps(x0_out, xbytes, noise, xbytes * (S0 - 1))) ||
+      overlaps(x0_out, xbytes, ws, L.total))
+    return fail(ARDIT_EINVAL, "x0_out overlaps x_init, noise or the workspace");
+
+  const int Lq = chunk_tokens(dims);
+  // pass i runs the streams with n_steps >= i (a prefix): denoising step i of
+  // those with n_steps > i, the commit pass (t = 0) of those with n_steps == i
+  for (int i = 0; i <= S0; ++i) {
+    int active = 0, denoise = 0;
+    float t[ARDIT_MAX_STREAMS];
+    SamplerArgs sa;
+    for (int b = 0; b < B; ++b) {
+      if (n_steps[b] >= i) active = b + 1;
+      if (n_steps[b] > i) denoise = b + 1;
+      const bool step = i < n_steps[b];
+      t[b] = step ? t_host[static_cast<size_t>(b) * t_ld + i] : 0.f;
+      sa.tau[b] = static_cast<float>(static_cast<double>(t[b]) / 1000.0);
+      sa.tau_next[b] = step && i + 1 < n_steps[b]
+          ? static_cast<float>(static_cast<double>(t_host[static_cast<size_t>(b) * t_ld + i + 1]) /
+                               1000.0)
+          : -1.f;
+    }
+    ardit_batch sb = *batch;
+    sb.n_streams = active;
+    ARDIT_TRY(time_mod_chain(stream, dims, active, t, tw, mod, ws, L));
+    const void* xin = i == 0 ? x_init : x0_out;
+    // a pass that only commits needs no output of its last layer
+    const bool commit_only = denoise == 0;
+    for (int l = 0; l < n_layers; ++l)
+      ARDIT_TRY(block_chain(stream, dims, &sb, l == 0 ? xin : vel, &kv[l], mod, ctx_k[l],
+                            ctx_v[l], &w[l], vel, ws, L, commit_only && l == n_layers - 1));
+    if (denoise > 0) {
+      sa.rows = denoise * Lq;
+      sa.rows_per_stream = Lq;
+      sa.vec_per_row = D / 8;
+      const bf16_t* eps = i + 1 < S0 ? static_cast<const bf16_t*>(noise) + i * N * D : nullptr;
+      ARDIT_HIP(launch_sampler(stream, static_cast<const bf16_t*>(xin), vel, eps,
+                               static_cast<bf16_t*>(x0_out), sa),
+                "sampler");
+    }
+  }
   return ARDIT_OK;
 }
 

@@ -195,4 +195,19 @@ hipError_t launch_linear_small(hipStream_t st, const float* x, int B, int K, con
                                const bf16_t* bias, int O, float* y, bool silu_in);
 hipError_t launch_time_sinusoid(hipStream_t st, const float* t_host, int B, float* s_out);
 
+// ------------------------------------------------------- chunk sampler
+// Rows [0, rows) of x, v, eps, out ([rows][vec_per_row * 8] bf16, stream
+// b = row / rows_per_stream): out = x0_hat = x - tau_b v when tau_next_b < 0,
+// else (1 - tau_next_b) x0_hat + tau_next_b eps (eps may then be null only if
+// no stream of the rows has tau_next >= 0).  out may alias x.
+struct SamplerArgs {
+  float tau[kMaxStreams];
+  float tau_next[kMaxStreams];
+  int32_t rows;
+  int32_t rows_per_stream;
+  int32_t vec_per_row;
+};
+hipError_t launch_sampler(hipStream_t st, const bf16_t* x, const bf16_t* v, const bf16_t* eps,
+                          bf16_t* out, const SamplerArgs& a);
+
 }  // namespace ardit

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     for code, name in A.STATUS.items():
         assert A.ardit_status_str(code) == name
     assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
-    assert A.ardit_version() == 400
+    assert A.ardit_version() == 500
 
 
 def _dims(**kw):
@@ -244,3 +244,63 @@ def test_mx_quantize_validation():
     assert _status(A.ardit_mx_quantize, FAKE, FAKE, 4, 48, 48, FAKE, FAKE) == -2
     assert _status(A.ardit_mx_quantize, FAKE, FAKE, 4, 64, 60, FAKE, FAKE) == -2
     assert _status(A.ardit_mx_quantize, FAKE, 0, 4, 64, 64, FAKE, FAKE) == -1
+
+
+# ------------------------------------------------ chunk generation (host side)
+def test_window_pages_match_oracle_listing():
+    """The C page-table policy equals the oracle's window listing and slot map
+    for every small (chunk, sink, window, frames) case, bit for bit."""
+    import itertools
+    import oracle as O
+    for c, sink, win, f in itertools.product(range(14), range(4), range(6), (1, 3)):
+        ids, cached = A.ardit_window_pages(c, sink, win, f, page_base=5)
+        ref, ref_cached = O.chunk_ref.window_page_table(c, sink, win, f)
+        assert cached == ref_cached and ids == [5 + int(v) for v in ref], (c, sink, win, f)
+        # slots of held chunks and of the chunk itself are distinct pages
+        assert len(set(ids)) == len(ids)
+        assert max(ids) < 5 + (sink + win + 1) * f
+
+
+def test_window_pages_rejections():
+    assert _status(A.ardit_window_pages, -1, 0, 1, 3) == -1
+    assert _status(A.ardit_window_pages, 0, 0, -1, 3) == -1
+    assert _status(A.ardit_window_pages, 0, 0, 1, 0) == -1
+    # table too short for 1 sink + 2 window chunks + the chunk (12 frames)
+    assert _status(A.ardit_window_pages, 5, 1, 2, 3, 0, 11) == -3
+    assert _status(A.ardit_window_pages, 5, 1, 2, 3, 2**31 - 10) == -3
+
+
+def _gen(n_steps=(2,), ts=((1000.0, 500.0),), x0=FAKE + (1 << 30), noise=FAKE, ws_bytes=None,
+         x_init=FAKE, dims=None, layers=2):
+    dims = dims or _dims()
+    B = len(n_steps)
+    b = A.Batch([192] * B, [384] * B, [6] * B, [32] * B)
+    need = A.ardit_workspace_size(dims, b) if ws_bytes is None else ws_bytes
+    A.ardit_chunk_generate(FAKE, dims, b, list(n_steps), [list(t) for t in ts], x_init, noise,
+                           [_kv()] * layers, A.time_weights({k: FAKE for k in A._TIME_FIELDS}),
+                           [FAKE] * layers, [FAKE] * layers, [_weights()] * layers, x0,
+                           FAKE + (1 << 34), need)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_steps=(1, 2), ts=((1000.0,), (1000.0, 500.0))), -1),   # steps increase along the batch
+    (dict(n_steps=(0,), ts=((),)), -1),                              # no step
+    (dict(n_steps=(17,), ts=((500.0,) * 17,)), -1),                  # above ARDIT_MAX_STEPS
+    (dict(ts=((1000.0, 1001.0),)), -1),                              # timestep outside [0, 1000]
+    (dict(ts=((float("nan"), 500.0),)), -1),
+    (dict(noise=None), -1),                                          # two steps need noise
+    (dict(x0=FAKE), -1),                                             # x0_out overlaps x_init
+    (dict(x0=FAKE + (1 << 34)), -1),                                 # x0_out overlaps the workspace
+    (dict(ws_bytes=1 << 20), -4),
+    (dict(layers=0), -1),
+])
+def test_chunk_generate_rejections(kw, code):
+    assert _status(lambda: _gen(**kw)) == code
+
+
+def test_workspace_holds_generation_buffers():
+    """The workspace grows by the velocity buffer and the modulation of the batch."""
+    d = _dims()
+    one = A.ardit_workspace_size(d, A.Batch([192], [384], [6], [32]))
+    two = A.ardit_workspace_size(d, A.Batch([192] * 2, [384] * 2, [6] * 2, [32] * 2))
+    assert two - one >= 2 * 192 * 256 * 2 + 6 * 256 * 4
