@@ -655,7 +655,7 @@ def test_sampler_step_closed_forms():
     x0 = rng.standard_normal((6, 8))
     eps = rng.standard_normal((6, 8))
     eps2 = rng.standard_normal((6, 8))
-    for t, tn in ((1000.0, 750.0), (750.0, 500.0), (250.0, None), (500.0, 0.0)):
+    for t, tn in ((1000.0, 750.0), (750.0, 500.0), (250.0, None), (500.0, 0.0), (750.0, 1000.0)):
         tau = t / 1000.0
         x = (1 - tau) * x0 + tau * eps
         v = eps - x0                       # the exact rectified-flow velocity
@@ -684,6 +684,15 @@ def test_window_listing_and_slots():
     # 3 (slot 3), then chunk 4 itself in slot 1 + 3 mod 3 = 1
     table, cached = CH.window_page_table(4, 1, 2, 3)
     assert cached == 9 and table.tolist() == [0, 1, 2, 6, 7, 8, 9, 10, 11, 3, 4, 5]
+    # a chunk inside the sink sees only the sink chunks before it, in its own slot
+    assert CH.window_chunks(1, 2, 3) == [0] and CH.chunk_slot(1, 2, 3) == 1
+    # a ring that wrapped: chunk 11, sink 2, window 3 holds 0, 1, 8, 9, 10 in
+    # slots 0, 1, 2 + 6 mod 4, 2 + 7 mod 4, 2 + 8 mod 4 and takes 2 + 9 mod 4
+    table, cached = CH.window_page_table(11, 2, 3, 1)
+    assert cached == 5 and table.tolist() == [0, 1, 4, 5, 2, 3]
+    # re-noising to tau' = 1 returns the fresh noise itself
+    e = np.arange(4.0)
+    assert np.array_equal(CH.sampler_step(np.ones(4), np.ones(4), 500.0, 1000.0, e), e)
 
 
 def test_sink_window_generation_equals_masked_full_sequence():
