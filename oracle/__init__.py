@@ -21,3 +21,4 @@ from .ardit_ref import (  # noqa: F401
 from . import sparse_ref  # noqa: F401
 from . import fp8_ref  # noqa: F401
 from . import chunk_ref  # noqa: F401
+from . import control_ref  # noqa: F401
