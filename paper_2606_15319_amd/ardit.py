@@ -75,6 +75,27 @@ class ardit_time_weights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in _TIME_FIELDS]
 
 
+class ardit_fidelity(C.Structure):
+    _fields_ = [("steps", C.c_int32), ("sparsity", C.c_float), ("window", C.c_int32),
+                ("quant", C.c_int32), ("latency_ms", C.c_double), ("quality", C.c_double)]
+
+
+class ardit_stream_state(C.Structure):
+    _fields_ = [("worker", C.c_int32), ("sp_donor", C.c_int32), ("slack_ms", C.c_double),
+                ("remaining_ms", C.c_double), ("cooldown_until_ms", C.c_double)]
+
+
+class ardit_ctl_params(C.Structure):
+    _fields_ = [("n_workers", C.c_int32), ("gpus_per_node", C.c_int32), ("cap_send", C.c_int32),
+                ("cap_recv", C.c_int32), ("cooldown_ms", C.c_double), ("now_ms", C.c_double)]
+
+
+class ardit_stream_decision(C.Structure):
+    _fields_ = [("cfg", C.c_int32), ("mode", C.c_int32), ("tier", C.c_int32),
+                ("queue_pos", C.c_int32), ("rehome_to", C.c_int32), ("sp_donor", C.c_int32),
+                ("credit_ms", C.c_double), ("cooldown_until_ms", C.c_double)]
+
+
 _vp, _i32, _sz = C.c_void_p, C.c_int32, C.c_size_t
 _P = C.POINTER
 _SIGS = {
@@ -106,6 +127,16 @@ _SIGS = {
                                        _P(C.c_float), _i32, _vp, _vp, _P(ardit_kv_paged),
                                        _P(ardit_time_weights), _P(_vp), _P(_vp),
                                        _P(ardit_block_weights), _vp, _vp, _sz]),
+    "ardit_pareto_frontier": (C.c_int, [_i32, _P(ardit_fidelity), _P(_i32), _P(_i32),
+                                        _P(C.c_double)]),
+    "ardit_bmpr_select": (C.c_int, [_i32, _P(ardit_fidelity), _i32, _P(_i32), C.c_double,
+                                    C.c_double, _P(_i32), _P(_i32)]),
+    "ardit_control_tick": (C.c_int, [_P(ardit_ctl_params), _i32, _P(ardit_fidelity), _i32,
+                                     _P(_i32), C.c_double, _i32, _P(ardit_stream_state),
+                                     _P(ardit_stream_decision)]),
+    "ardit_evict_for": (C.c_int, [_i32, _P(C.c_double), _P(_i32), _i32, C.c_int64, C.c_int64,
+                                  _P(_i32), _P(_i32)]),
+    "ardit_admit": (C.c_int, [_i32, _P(_i32), C.c_double, _P(_i32), _P(C.c_double)]),
     "ardit_timing_enable": (C.c_int, [C.c_int]),
     "ardit_timing_collect": (C.c_int, [_P(_i32), _P(C.c_double)]),
 }
@@ -332,3 +363,77 @@ def ardit_timing_collect():
     ms = C.c_double(0.0)
     _check(_lib.ardit_timing_collect(C.byref(n), C.byref(ms)), "ardit_timing_collect")
     return n.value, ms.value
+
+
+# ------------------------------------------------------------- controller
+URGENT, NORMAL, RELAXED = 0, 1, 2
+BMPR_QUALITY, BMPR_SPEED_RECOVERY = 0, 1
+
+
+def fidelity_array(cfgs):
+    """cfgs: sequence of (steps, sparsity, window, quant, latency_ms, quality)."""
+    arr = (ardit_fidelity * len(cfgs))()
+    for i, c in enumerate(cfgs):
+        arr[i] = ardit_fidelity(int(c[0]), float(c[1]), int(c[2]), int(c[3]), float(c[4]),
+                                float(c[5]))
+    return arr
+
+
+def ardit_pareto_frontier(cfgs):
+    """Returns (frontier indices, quality floor)."""
+    arr = cfgs if isinstance(cfgs, C.Array) else fidelity_array(cfgs)
+    n = len(arr)
+    f = (C.c_int32 * n)()
+    m = C.c_int32(0)
+    fl = C.c_double(0.0)
+    _check(_lib.ardit_pareto_frontier(n, arr, f, C.byref(m), C.byref(fl)), "ardit_pareto_frontier")
+    return [f[i] for i in range(m.value)], fl.value
+
+
+def ardit_bmpr_select(cfgs, frontier, q_floor, budget_ms):
+    arr = cfgs if isinstance(cfgs, C.Array) else fidelity_array(cfgs)
+    f = (C.c_int32 * len(frontier))(*frontier)
+    c, m = C.c_int32(0), C.c_int32(0)
+    _check(_lib.ardit_bmpr_select(len(arr), arr, len(frontier), f, float(q_floor),
+                                  float(budget_ms), C.byref(c), C.byref(m)), "ardit_bmpr_select")
+    return c.value, m.value
+
+
+def ardit_control_tick(params: dict, cfgs, frontier, q_floor, streams):
+    """params: n_workers, gpus_per_node, cap_send, cap_recv, cooldown_ms, now_ms;
+    streams: sequence of (worker, sp_donor, slack_ms, remaining_ms, cooldown_until_ms).
+    Returns a list of ardit_stream_decision."""
+    p = ardit_ctl_params(int(params["n_workers"]), int(params.get("gpus_per_node", 8)),
+                         int(params.get("cap_send", 2)), int(params.get("cap_recv", 1)),
+                         float(params.get("cooldown_ms", 60000.0)), float(params.get("now_ms", 0.0)))
+    arr = cfgs if isinstance(cfgs, C.Array) else fidelity_array(cfgs)
+    f = (C.c_int32 * len(frontier))(*frontier)
+    n = len(streams)
+    st = (ardit_stream_state * max(n, 1))()
+    for i, s in enumerate(streams):
+        st[i] = ardit_stream_state(int(s[0]), int(s[1]), float(s[2]), float(s[3]), float(s[4]))
+    out = (ardit_stream_decision * max(n, 1))()
+    _check(_lib.ardit_control_tick(C.byref(p), len(arr), arr, len(frontier), f, float(q_floor), n,
+                                   st, out), "ardit_control_tick")
+    return [out[i] for i in range(n)]
+
+
+def ardit_evict_for(credits, resident_pages, requester, free_pages, need_pages):
+    """Evicted stream indices in order; raises ArditError (ARDIT_ECAPACITY) when
+    the pages cannot fit."""
+    n = len(credits)
+    c = (C.c_double * max(n, 1))(*[float(v) for v in credits])
+    r = (C.c_int32 * max(n, 1))(*[int(v) for v in resident_pages])
+    ev = (C.c_int32 * max(n, 1))()
+    m = C.c_int32(0)
+    _check(_lib.ardit_evict_for(n, c, r, int(requester), int(free_pages), int(need_pages), ev,
+                                C.byref(m)), "ardit_evict_for")
+    return [ev[i] for i in range(m.value)]
+
+
+def ardit_admit(streams_per_worker, first_chunk_ms):
+    n = len(streams_per_worker)
+    a = (C.c_int32 * n)(*[int(v) for v in streams_per_worker])
+    h, sl = C.c_int32(0), C.c_double(0.0)
+    _check(_lib.ardit_admit(n, a, float(first_chunk_ms), C.byref(h), C.byref(sl)), "ardit_admit")
+    return h.value, sl.value

@@ -693,6 +693,11 @@ int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
 
 }  // namespace
 
+namespace ardit {
+// the calling thread's error detail, for the controller's translation unit
+int set_error(int status, const char* msg) { return fail(status, "%s", msg); }
+}  // namespace ardit
+
 // ======================================================================== ABI
 extern "C" {
 

@@ -11,13 +11,13 @@ import pytest
 A = pytest.importorskip("paper_2606_15319_amd.ardit",
                         reason="libardit.so not built (python -m paper_2606_15319_amd.build)")
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                      "include", "ardit.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = [os.path.join(INCLUDE, f) for f in sorted(os.listdir(INCLUDE)) if f.endswith(".h")]
 FAKE = 1 << 20   # 16-byte aligned stand-in address, never dereferenced
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(ardit_[a-z_]+)\s*\(", text)))
 
