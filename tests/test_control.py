@@ -127,3 +127,21 @@ def test_controller_rejections():
     assert _status(A.ardit_control_tick, p, cfgs, f, fl, [(0, -1, math.inf, 0.0, -math.inf)]) == -1
     assert _status(A.ardit_control_tick, dict(n_workers=0), cfgs, f, fl, []) == -1
     assert _status(A.ardit_admit, [], 10.0) == -1
+
+
+def test_profiler_space_is_the_papers():
+    """The profiler enumerates the 90 configurations of the paper's knob
+    product (golden settings, Appendix A), the reference first, with S
+    timesteps spaced evenly from 1000."""
+    import itertools
+    import json
+    import os
+    from paper_2606_15319_amd import profiler as P
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_settings.json")))
+    space = list(itertools.product(P.STEPS, P.SPARSITY, P.WINDOWS, P.QUANTS))
+    assert len(space) == g["n_fidelity_configs"] == 90
+    assert list(P.STEPS) == g["denoise_steps"] and list(P.SPARSITY) == g["sparsity"]
+    assert list(P.WINDOWS) == g["kv_window_chunks"] and len(P.QUANTS) == len(g["quant_modes"])
+    top = g["top_config"]
+    assert P.REFERENCE == (top[0], top[1], top[2], g["quant_modes"].index(top[3]))
+    assert P.timesteps(4) == [1000.0, 750.0, 500.0, 250.0] and P.timesteps(2) == [1000.0, 500.0]
