@@ -25,6 +25,8 @@ difference of two stored tensors that nearly cancel (with random weights the
 stack is close to the identity, so v ~ x): a flip in x or v carries their
 ulp, not x0's, so its quantum is |x| + tau |v| of the last step.
 """
+import math
+
 import numpy as np
 import pytest
 
@@ -257,3 +259,90 @@ def test_chunk_chain_sink_window_tracks_oracle(A):
                              quantum=kv_ref[l][0], half_ulps=k_ulps))
                 print(parity(v_got, kv_ref[l][1], f"chunk {c} stream {b} layer {l} committed v",
                              quantum=kv_ref[l][1], half_ulps=k_ulps))
+
+
+def test_controller_drives_batched_generation(A):
+    """The controller picks each stream's configuration (BMPR over a latency
+    table) and the streams then generate their chunks in one batched call
+    with those step counts and windows (streams ordered by steps, as the
+    call requires); every stream tracks its own float64 oracle run."""
+    import torch
+    n_layers = 2
+    F = SH.frames
+    # (S, rho, W, Q, ms per chunk, quality): a synthetic table; the median
+    # quality (the floor) is 75
+    table = [(4, 0.0, 3, 0, 300.0, 90.0), (4, 0.0, 1, 0, 220.0, 85.0),
+             (3, 0.0, 3, 0, 200.0, 84.0), (3, 0.0, 1, 0, 150.0, 80.0),
+             (2, 0.0, 3, 0, 130.0, 70.0), (2, 0.0, 1, 0, 100.0, 60.0),
+             (2, 0.0, 7, 0, 400.0, 50.0), (3, 0.0, 7, 0, 500.0, 55.0)]
+    frontier, floor = A.ardit_pareto_frontier(table)
+    assert floor == 75.0
+    # budget 210 ms: (3, 3) fits; 1000 ms: the best (4, 3); 40 ms: nothing fits,
+    # speed recovery takes the fastest point above the floor, (3, 1)
+    streams = [(0, -1, 210.0, 0.0, -math.inf), (0, -1, 1000.0, 0.0, -math.inf),
+               (0, -1, 50.0, 10.0, -math.inf)]
+    dec = A.ardit_control_tick(dict(n_workers=1), table, frontier, floor, streams)
+    cfg = [table[d.cfg] for d in dec]
+    assert [d.cfg for d in dec] == [2, 0, 3]
+    assert [d.mode for d in dec] == [A.BMPR_QUALITY, A.BMPR_QUALITY, A.BMPR_SPEED_RECOVERY]
+    assert [d.tier for d in dec] == [A.URGENT, A.NORMAL, A.URGENT]
+    assert [d.queue_pos for d in dec] == [1, 2, 0]
+    order = sorted(range(3), key=lambda b: -cfg[b][0])        # non-increasing steps
+    m = Model(A, 92, n_layers, [32, 32, 32])
+    rng = m.rng
+    chunk_idx = [5, 4, 6]
+    slots = max(t[2] for t in table) + 1
+    ids_all, cached_all, held_all = [], [], []
+    for pos, b in enumerate(order):
+        W = cfg[b][2]
+        ids, cached = A.ardit_window_pages(chunk_idx[b], 0, W, F, pos * slots * F)
+        ids_all.append(ids)
+        cached_all.append(cached)
+        held_all.append(O.chunk_ref.window_chunks(chunk_idx[b], 0, W))
+    n_pages = 3 * slots * F
+    pools = [PagedCache(SH, ids_all, n_pages) for _ in range(n_layers)]
+    caches = [[None] * n_layers for _ in order]
+    for l, p in enumerate(pools):
+        for pos in range(3):
+            n = cached_all[pos] * SH.tokens_per_frame
+            k = normal_bf16(rng, (n, SH.n_heads, SH.head_dim))
+            v = normal_bf16(rng, (n, SH.n_heads, SH.head_dim))
+            if n:
+                p.fill_stream(pos, k, v)
+            caches[pos][l] = (k, v)
+        p.upload()
+    B = 3
+    steps = [cfg[b][0] for b in order]
+    ts = [[1000.0 * (1 - i / s) for i in range(s)] for s in steps]
+    x_init = [normal_bf16(rng, (LQ, SH.dim)) for _ in range(B)]
+    noise = [[normal_bf16(rng, (LQ, SH.dim)) for _ in range(s - 1)] for s in steps]
+    noise_dev = np.zeros((max(steps) - 1, B * LQ, SH.dim), dtype=np.float32)
+    for pos in range(B):
+        for i, e in enumerate(noise[pos]):
+            noise_dev[i, pos * LQ:(pos + 1) * LQ] = e
+    batch = A.Batch([LQ] * B, [c * SH.tokens_per_frame for c in cached_all],
+                    [F * chunk_idx[b] for b in order], m.ctx_lens)
+    ws, ws_bytes = m.workspace(batch)
+    x0 = torch.empty((B * LQ, SH.dim), dtype=torch.bfloat16, device="cuda")
+    A.ardit_chunk_generate(None, m.dims, batch, steps, ts, dev_bf16(np.concatenate(x_init)),
+                           dev_bf16(noise_dev), [p.kv(A) for p in pools], m.tw, m.ctx_k, m.ctx_v,
+                           m.w, x0, ws, ws_bytes)
+    _sync()
+    got = host_f32(x0)
+    for pos, b in enumerate(order):
+        x0_ref, kv_ref, xs_ref = O.chunk_ref.generate_chunk(
+            x_init[pos], noise[pos], ts[pos], caches[pos], F * chunk_idx[b], m.time_w,
+            m.ctx_ref[pos], m.block_w, SH, store=bf16_round)
+        tau = ts[pos][-1] / 1000.0
+        v_last = (xs_ref[-1] - x0_ref) / tau
+        k_ulps = 2.0 * np.sqrt(n_layers * (steps[pos] + 1) * (len(held_all[pos]) + 1))
+        print(parity(got[pos * LQ:(pos + 1) * LQ], x0_ref,
+                     f"stream {b} (S={steps[pos]}, W={cfg[b][2]}) x0",
+                     quantum=np.abs(xs_ref[-1]) + tau * np.abs(v_last), half_ulps=k_ulps))
+        own = ids_all[pos][cached_all[pos]:][:F]
+        for l, p in enumerate(pools):
+            kb, vb = p.device_bits()
+            k_got = np.transpose(bits_to_f32(kb[own]), (0, 2, 1, 3)).reshape(LQ, SH.n_heads,
+                                                                             SH.head_dim)
+            print(parity(k_got, kv_ref[l][0], f"stream {b} layer {l} committed k",
+                         quantum=kv_ref[l][0], half_ulps=k_ulps))
