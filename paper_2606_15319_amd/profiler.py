@@ -17,6 +17,12 @@ FP16) on the same starting noise, weights and cache -- how far the
 configuration moves the output, not how good it looks.
 
 Run: python -m paper_2606_15319_amd.profiler --out result.json [--md summary.md]
+
+--controller PROFILE times the host controller instead (no GPU): one
+ardit_control_tick over the frontier of a profile written by the run above
+(its JSON, or the table of its markdown summary),
+for 64 to 4096 streams with random slack on 16 or 64 workers (the paper
+measures its controller's latency against the stream count, Appendix D.1).
 """
 from __future__ import annotations
 
@@ -178,18 +184,71 @@ def markdown(res, command):
     for i in order:
         r = rows[i]
         lines.append(f"| {r['steps']} | {r['sparsity']} | {r['window']} | "
-                     f"{'FP8' if r['quant'] else 'FP16'} | {r['latency_ms']:.1f} | "
-                     f"{r['quality']:.4f} | {'*' if i in fr else ''} |")
+                     f"{'FP8' if r['quant'] else 'FP16'} | {r['latency_ms']:.3f} | "
+                     f"{r['quality']:.6f} | {'*' if i in fr else ''} |")
     return "\n".join(lines) + "\n"
+
+
+def read_profile(path):
+    """(S, rho, W, Q, ms per chunk, quality) rows from a profile: the JSON this
+    module writes, or the table of its markdown summary."""
+    if path.endswith(".json"):
+        with open(path) as f:
+            return [(r["steps"], r["sparsity"], r["window"], r["quant"], r["latency_ms"],
+                     r["quality"]) for r in json.load(f)["configs"]]
+    import re
+    rows = []
+    pat = re.compile(r"\| (\d) \| ([0-9.]+) \| (\d) \| (FP16|FP8) \| ([0-9.]+) \| (-?[0-9.]+) \|")
+    with open(path) as f:
+        for line in f:
+            m = pat.match(line)
+            if m:
+                rows.append((int(m[1]), float(m[2]), int(m[3]), int(m[4] == "FP8"), float(m[5]),
+                             float(m[6])))
+    return rows
+
+
+def controller_latency(profile_json, reps=200, seed=0):
+    """Microseconds per control tick for several (streams, workers) sizes."""
+    import ctypes as C
+    import math
+    import random
+    from paper_2606_15319_amd import ardit as A
+    cfgs = A.fidelity_array(read_profile(profile_json))
+    frontier, floor = A.ardit_pareto_frontier(cfgs)
+    fr = (C.c_int32 * len(frontier))(*frontier)
+    rnd = random.Random(seed)
+    out = []
+    for U, G in ((64, 16), (256, 16), (1024, 16), (4096, 64)):
+        st = (A.ardit_stream_state * U)(*[
+            A.ardit_stream_state(rnd.randrange(G), -1, rnd.uniform(-200.0, 3000.0),
+                                 rnd.uniform(0.0, 200.0), -math.inf) for _ in range(U)])
+        dec = (A.ardit_stream_decision * U)()
+        p = A.ardit_ctl_params(G, 8, 2, 1, 60000.0, 0.0)
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            if A._lib.ardit_control_tick(C.byref(p), len(cfgs), cfgs, len(frontier), fr, floor, U,
+                                         st, dec) != 0:
+                raise RuntimeError(A.ardit_last_error())
+        us = (time.perf_counter() - t0) / reps * 1e6
+        out.append(dict(streams=U, workers=G, frontier=len(frontier), us_per_tick=round(us, 1)))
+        log(f"{U} streams on {G} workers, frontier {len(frontier)}: {us:.1f} us per tick")
+    return out
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--layers", type=int, default=30)
     ap.add_argument("--reps", type=int, default=2)
-    ap.add_argument("--out", required=True)
+    ap.add_argument("--out", default=None)
     ap.add_argument("--md", default=None)
+    ap.add_argument("--controller", default=None, metavar="PROFILE")
     a = ap.parse_args()
+    if a.controller:
+        print(json.dumps(controller_latency(a.controller)))
+        return
+    if not a.out:
+        ap.error("--out is required")
     t0 = time.time()
     res = profile(a.layers, a.reps)
     with open(a.out, "w") as f:

@@ -145,3 +145,30 @@ def test_profiler_space_is_the_papers():
     top = g["top_config"]
     assert P.REFERENCE == (top[0], top[1], top[2], g["quant_modes"].index(top[3]))
     assert P.timesteps(4) == [1000.0, 750.0, 500.0, 250.0] and P.timesteps(2) == [1000.0, 500.0]
+
+
+def test_committed_profile_frontier_is_consistent():
+    """The MI355X latency table under profiles/ covers the 90 configurations
+    and its starred rows are exactly the frontier ardit_pareto_frontier
+    builds from it (and the oracle's definition agrees)."""
+    import itertools
+    import os
+    from paper_2606_15319_amd import profiler as P
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "profiles",
+                        "fidelity_block13b_latency.md")
+    rows = P.read_profile(path)
+    assert sorted((r[0], r[1], r[2], r[3]) for r in rows) == \
+        sorted(itertools.product(P.STEPS, P.SPARSITY, P.WINDOWS, P.QUANTS))
+    starred = []
+    for line in open(path):
+        if line.startswith("| ") and line.rstrip().endswith("| * |"):
+            starred.append(line)
+    f, fl = A.ardit_pareto_frontier(rows)
+    assert len(f) == len(starred)
+    assert f == K.pareto_frontier([r[4] for r in rows], [r[5] for r in rows])
+    assert fl == K.quality_floor([r[5] for r in rows])
+    # every starred row is a frontier row
+    on = {(rows[i][0], rows[i][1], rows[i][2], rows[i][3]) for i in f}
+    for line in starred:
+        c = [x.strip() for x in line.strip().strip("|").split("|")]
+        assert (int(c[0]), float(c[1]), int(c[2]), int(c[3] == "FP8")) in on
