@@ -63,15 +63,24 @@ __device__ __forceinline__ float mx_inv_scale(int e) {
   return __uint_as_float(static_cast<uint32_t>(127 - e) << 23);
 }
 
+// floor(log2 amax) - 7 clamped to [-127, 127], -127 for 0, without branches
+// (the exponent instruction handles subnormal inputs); amax >= 0 and finite
+__device__ __forceinline__ int mx_exponent_nb(float amax) {
+  const int e = __builtin_amdgcn_frexp_expf(amax) - 8;
+  return amax > 0.f ? min(max(e, -127), 127) : -127;
+}
+
 // max of x over lanes l and l ^ 32 (one swap of the wave's halves, no LDS)
 __device__ __forceinline__ float half_pair_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// four floats (|x| < 256) -> four E4M3 bytes, first value in the low byte
+// four floats (|x| < 256) -> four E4M3 bytes, first value in the low byte (the
+// first conversion's untouched half is overwritten by the second, so it starts
+// from a's bits instead of a zeroed register)
 __device__ __forceinline__ uint32_t pack4_e4m3(float a, float b, float c, float d) {
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, __float_as_int(a), false);
   w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
   return static_cast<uint32_t>(w);
 }
@@ -373,8 +382,8 @@ __global__ __launch_bounds__(F8_NTHR, 1) void attn_fp8_kernel(const AttnArgs a) 
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
     }
-    const int e0 = mx_exponent(__builtin_amdgcn_exp2f(fmaf(sb0, c, -m_run)));
-    const int e1 = mx_exponent(__builtin_amdgcn_exp2f(fmaf(sb1, c, -m_run)));
+    const int e0 = mx_exponent_nb(__builtin_amdgcn_exp2f(fmaf(sb0, c, -m_run)));
+    const int e1 = mx_exponent_nb(__builtin_amdgcn_exp2f(fmaf(sb1, c, -m_run)));
     const float m0 = m_run + static_cast<float>(e0), m1 = m_run + static_cast<float>(e1);
     float ps0 = 0.f, ps1 = 0.f;   // block sums of the scaled weights
 #pragma unroll
