@@ -468,6 +468,62 @@ __global__ __launch_bounds__(256) void v_transpose_kernel(const VtParams p) {
   for (int dd = threadIdx.x >> 6; dd < p.hd; dd += 4) dst[static_cast<size_t>(dd) * T] = tile[r][dd];
 }
 
+// Paged value append with 16-byte stores: 64 tokens x one head staged in LDS
+// (16-byte chunk cc of token r at slot cc ^ ((r / 8) % 8), so the eight
+// lanes gathering one dim from eight 8-token groups hit distinct banks); a
+// lane then gathers 8 consecutive tokens of one dim and stores them as one
+// 16-byte write, eight lanes filling 128 contiguous bytes of a transposed row
+// (69 against 71 us for the 2-byte stores at 37440 rows; 256-token tiles were
+// slower, 105 us).  Transposed rows are T = 1560 tokens long, so these 128-byte
+// pieces straddle cache lines: a row pitch rounded to 64 tokens would align
+// them, at the price of a page layout change.
+// Needs every stream's rows and cache length in multiples of 8 and T % 8 == 0,
+// so each 8-token group lies in one stream and one page.
+constexpr int kVaRows = 64;
+
+__global__ __launch_bounds__(256) void v_append16_kernel(const VtParams p) {
+  __shared__ __attribute__((aligned(16))) bf16_t tile[kVaRows][128];
+  const int n0 = blockIdx.x * kVaRows;
+  const int h = blockIdx.y;
+  const int cpr = p.hd >> 3;  // 16-byte chunks per row of one head
+  for (int c = threadIdx.x; c < kVaRows * cpr; c += 256) {
+    const int r = c / cpr, cc = c - r * cpr;
+    const int n = n0 + r;
+    if (n < p.N) {
+      const uint4 u = *reinterpret_cast<const uint4*>(
+          p.src + static_cast<size_t>(n) * p.ld_src + p.col_off + h * p.hd + cc * 8);
+      *reinterpret_cast<uint4*>(&tile[r][8 * (cc ^ ((r >> 3) & 7))]) = u;
+    }
+  }
+  __syncthreads();
+  // item (dim dd, group g): lanes of one dim take consecutive groups
+  for (int it = threadIdx.x; it < p.hd * (kVaRows / 8); it += 256) {
+    const int g = it & (kVaRows / 8 - 1), dd = it / (kVaRows / 8);
+    const int r0 = 8 * g;
+    const int n = n0 + r0;
+    if (n >= p.N) continue;
+    const int b = find_stream(p.rs, n);
+    const RowStream s = p.rs.s[b];
+    const int slot = s.cache_len + n - s.row_begin;
+    const int fr = static_cast<int>(fdiv(static_cast<uint32_t>(slot), p.fT));
+    const int page =
+        clamp_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr], p.n_pages);
+    const int off = slot - fr * p.T;
+    const int cc = dd >> 3, e = dd & 7;
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int ra = r0 + 2 * k, rb = ra + 1;
+      const uint32_t lo = tile[ra][8 * (cc ^ ((ra >> 3) & 7)) + e];
+      const uint32_t hi = tile[rb][8 * (cc ^ ((rb >> 3) & 7)) + e];
+      w[k] = lo | (hi << 16);
+    }
+    bf16_t* dst = p.dst + (static_cast<size_t>(page) * p.H + h) * p.hd * p.T +
+                  static_cast<size_t>(dd) * p.T + off;
+    *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int col_off, int N,
                               int D, int H, int hd, bf16_t* dst, bool paged, int T,
                               const int32_t* page_table, int max_frames, int n_pages,
@@ -489,8 +545,15 @@ hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int
   p.n_pages = n_pages;
   p.page_table = page_table;
   p.rs = rs;
-  hipLaunchKernelGGL(v_transpose_kernel, dim3((N + kVtRows - 1) / kVtRows, H), dim3(256), 0, st,
-                     p);
+  bool groups8 = paged && T % 8 == 0 && hd <= 128 && N % 8 == 0;
+  for (int i = 0; i < rs.n && groups8; ++i)
+    groups8 = rs.s[i].len % 8 == 0 && rs.s[i].cache_len % 8 == 0 && rs.s[i].row_begin % 8 == 0;
+  if (groups8)
+    hipLaunchKernelGGL(v_append16_kernel, dim3((N + kVaRows - 1) / kVaRows, H), dim3(256), 0, st,
+                       p);
+  else
+    hipLaunchKernelGGL(v_transpose_kernel, dim3((N + kVtRows - 1) / kVtRows, H), dim3(256), 0,
+                       st, p);
   return hipGetLastError();
 }
 
