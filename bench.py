@@ -260,6 +260,39 @@ def cpu_baseline(model):
                        f"({(t_ctx - t0) * 1e3:.0f} ms) excluded as on the GPU path")}
 
 
+def kernel_breakdown(A, model, args, sh, cache_lens):
+    """One more step, outside the timed region, with events around every GEMM
+    and elementwise launch: their rates against the MFMA and HBM peaks.
+    GEMM work per block 2 N D (6 D + 2 F) flops (QKV, O, cross-Q, cross-O,
+    FFN up and down); elementwise bytes per block 32 N D (each input read once,
+    each output written once, bf16 2 bytes and fp32 4: adaLN from bf16 4ND,
+    QK-norm/RoPE/key append 8ND, value append 4ND, cross pre-norm from fp32
+    6ND, cross q-norm 4ND, adaLN from fp32 6ND)."""
+    import torch
+    A.ardit_timing_enable((1 << A.TIME_GEMM) | (1 << A.TIME_ELEMENTWISE))
+    model.step(args.steps)
+    torch.cuda.synchronize()
+    A.ardit_timing_enable(False)
+    ng, gms = A.ardit_timing_collect_kind(A.TIME_GEMM)
+    ne, ems = A.ardit_timing_collect_kind(A.TIME_ELEMENTWISE)
+    N, D, F = sh.chunk_tokens * len(cache_lens), sh.dim, sh.ffn_dim
+    blocks = args.layers
+    gflop = 2.0 * N * D * (6 * D + 2 * F) * blocks / 1e9
+    ebytes = 32.0 * N * D * blocks
+    g_tf = gflop / (gms * 1e-3) / 1e3
+    e_tb = ebytes / (ems * 1e-3) / 1e12
+    log(f"GEMMs {gms / blocks:.3f} ms/block ({g_tf:.0f} TFLOP/s over {ng} launches), "
+        f"elementwise {ems / blocks:.3f} ms/block ({e_tb:.2f} TB/s over {ne} launches)")
+    return {"gemm": {"ms_per_block": round(gms / blocks, 4), "achieved": round(g_tf, 1),
+                     "unit": "TFLOP/s", "peak": PEAK_BF16_TFLOPS,
+                     "frac": round(g_tf / PEAK_BF16_TFLOPS, 4), "launches": ng},
+            "elementwise": {"ms_per_block": round(ems / blocks, 4), "achieved": round(e_tb, 3),
+                            "unit": "TB/s", "peak": 8.0, "frac": round(e_tb / 8.0, 4),
+                            "launches": ne},
+            "note": "one extra step with events around each GEMM and elementwise launch, "
+                    "outside the timed region"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -328,6 +361,9 @@ def main():
     achieved = attn_flops / (attn_avg_ms * 1e-3) / 1e12
     log(f"{ms_step:.3f} ms/step, {ms_block:.4f} ms/block pass, attention {attn_avg_ms:.4f} ms "
         f"({achieved:.1f} TFLOP/s) over {n_attn} launches")
+    breakdown = None
+    if not args.chunk:
+        breakdown = kernel_breakdown(A, model, args, sh, cache_lens)
     cpu = None
     if not args.no_cpu_baseline and not ragged:
         log("timing the CPU oracle on one block step")
@@ -383,6 +419,7 @@ def main():
                                 + ("block-sparse " if args.sparsity else "")
                                 + "paged self-attention"),
                      "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},
+        "breakdown": breakdown,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -314,13 +314,22 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
                          const void* const* ctx_k, const void* const* ctx_v,
                          const ardit_block_weights* w, void* x0_out, void* ws, size_t ws_bytes);
 
-/* Kernel timing: while enabled, block calls record HIP events on their stream
- * around every launch of the self-attention kernel (for sparse streams the
- * attention over the kept tiles, after the block selection).  ardit_timing_collect
- * waits for the recorded events, returns the number of launches and their
- * summed duration in ms, and clears the record. */
+/* Kernel timing.  ardit_timing_enable(mask) turns on HIP events recorded on
+ * the launch stream around each launch of the kinds in mask: bit 0 (1) the
+ * self-attention kernel (for sparse streams the attention over the kept
+ * tiles, after the block selection; for FP8 streams the FP8 attention after
+ * its quantisation pre-pass), bit 1 (2) the block's six GEMMs, bit 2 (4) its
+ * elementwise kernels (both adaLN norms, both RMS-gain norms, QK-norm / RoPE /
+ * key append, value append); 0 turns timing off.  The events of the GEMM and
+ * elementwise kinds sit between kernels that otherwise follow each other on
+ * the stream, so timing them can add small gaps.  ardit_timing_collect_kind
+ * waits for the recorded events of one kind (0, 1 or 2), returns the number of
+ * launches and their summed duration in ms, and clears that kind's record;
+ * ardit_timing_collect is the same for kind 0.  ARDIT_EINVAL for a mask or
+ * kind out of range. */
 int ardit_timing_enable(int enable);
 int ardit_timing_collect(int32_t* launches, double* total_ms);
+int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms);
 
 #ifdef __cplusplus
 }

@@ -139,6 +139,7 @@ _SIGS = {
     "ardit_admit": (C.c_int, [_i32, _P(_i32), C.c_double, _P(_i32), _P(C.c_double)]),
     "ardit_timing_enable": (C.c_int, [C.c_int]),
     "ardit_timing_collect": (C.c_int, [_P(_i32), _P(C.c_double)]),
+    "ardit_timing_collect_kind": (C.c_int, [_i32, _P(_i32), _P(C.c_double)]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -354,8 +355,21 @@ def ardit_chunk_generate(stream, dims, batch: Batch, n_steps, timesteps, x_init,
            "ardit_chunk_generate")
 
 
-def ardit_timing_enable(enable: bool):
-    _check(_lib.ardit_timing_enable(1 if enable else 0), "ardit_timing_enable")
+TIME_ATTENTION, TIME_GEMM, TIME_ELEMENTWISE = 0, 1, 2
+
+
+def ardit_timing_enable(enable):
+    """enable: a bool (attention launches only) or a mask of 1 << TIME_* bits."""
+    mask = int(enable) if not isinstance(enable, bool) else (1 if enable else 0)
+    _check(_lib.ardit_timing_enable(mask), "ardit_timing_enable")
+
+
+def ardit_timing_collect_kind(kind):
+    n = C.c_int32(0)
+    ms = C.c_double(0.0)
+    _check(_lib.ardit_timing_collect_kind(int(kind), C.byref(n), C.byref(ms)),
+           "ardit_timing_collect_kind")
+    return n.value, ms.value
 
 
 def ardit_timing_collect():

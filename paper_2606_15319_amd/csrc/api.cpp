@@ -357,11 +357,19 @@ RowStreams ctx_streams(const ardit_batch* b) {
 }
 
 // ---------------------------------------------------------------- timing
+// kinds of timed launches (bits of the enable mask)
+enum TimedKind : int { kTimeAttn = 0, kTimeGemm = 1, kTimeElem = 2, kTimeKinds = 3 };
+
+struct TimedRec {
+  int kind;
+  hipEvent_t e0, e1;
+};
+
 struct Timing {
   std::mutex mu;
-  bool enabled = false;
+  unsigned mask = 0;
   std::vector<hipEvent_t> pool;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> rec;
+  std::vector<TimedRec> rec;
 };
 Timing& timing() {
   static Timing t;
@@ -379,29 +387,47 @@ hipEvent_t take_event(Timing& t) {
   return e;
 }
 
-// launches the self-attention kernels (block selection first when sparse);
-// while timing is on, events bracket the attention kernel itself
-int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
-  Timing& tm = timing();
+// Events around one launch while timing of its kind is on: begin() before
+// the launch, end() after it.
+struct TimedLaunch {
+  hipStream_t st;
+  int kind;
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  {
+  TimedLaunch(hipStream_t s, int k) : st(s), kind(k) {
+    Timing& tm = timing();
     std::lock_guard<std::mutex> g(tm.mu);
-    if (tm.enabled) {
+    if (tm.mask & (1u << k)) {
       e0 = take_event(tm);
       e1 = take_event(tm);
     }
   }
-  if (a.blocks) ARDIT_HIP(launch_sparse_select(st, a, hd), "block selection launch");
-  if (e0 && e1) ARDIT_HIP(hipEventRecord(e0, st), "hipEventRecord");
-  if (a.blocks)
-    ARDIT_HIP(launch_sparse_attention(st, a, hd), "block-sparse attention launch");
-  else
-    ARDIT_HIP(launch_attention(st, a, hd, true), "self-attention launch");
-  if (e0 && e1) {
-    ARDIT_HIP(hipEventRecord(e1, st), "hipEventRecord");
+  hipError_t begin() { return e0 && e1 ? hipEventRecord(e0, st) : hipSuccess; }
+  hipError_t end() {
+    if (!(e0 && e1)) return hipSuccess;
+    const hipError_t e = hipEventRecord(e1, st);
+    Timing& tm = timing();
     std::lock_guard<std::mutex> g(tm.mu);
-    tm.rec.emplace_back(e0, e1);
+    tm.rec.push_back(TimedRec{kind, e0, e1});
+    return e;
   }
+};
+
+#define ARDIT_TIMED(kind, expr, what)                              \
+  do {                                                             \
+    TimedLaunch tl_(st, kind);                                     \
+    ARDIT_HIP(tl_.begin(), "hipEventRecord");                      \
+    ARDIT_HIP(expr, what);                                         \
+    ARDIT_HIP(tl_.end(), "hipEventRecord");                        \
+  } while (0)
+
+// launches the self-attention kernels (block selection first when sparse);
+// while timing is on, events bracket the attention kernel itself
+int run_self_attention(hipStream_t st, const AttnArgs& a, int hd) {
+  if (a.blocks) ARDIT_HIP(launch_sparse_select(st, a, hd), "block selection launch");
+  if (a.blocks)
+    ARDIT_TIMED(kTimeAttn, launch_sparse_attention(st, a, hd), "block-sparse attention launch");
+  else
+    ARDIT_TIMED(kTimeAttn, launch_attention(st, a, hd, true), "self-attention launch");
   return ARDIT_OK;
 }
 
@@ -504,22 +530,7 @@ int self_attention(hipStream_t st, const ardit_dims* d, const ardit_batch* b, co
     ARDIT_HIP(launch_mx_quantize_rows(st, static_cast<const bf16_t*>(q), sum_q(b), d->dim, d->dim,
                                       a8.q8, a8.q8s), "FP8 query quantisation");
     ARDIT_HIP(launch_fp8_kv_prep(st, a8, hd), "FP8 key / value quantisation");
-    Timing& tm = timing();
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    {
-      std::lock_guard<std::mutex> g(tm.mu);
-      if (tm.enabled) {
-        e0 = take_event(tm);
-        e1 = take_event(tm);
-      }
-    }
-    if (e0 && e1) ARDIT_HIP(hipEventRecord(e0, st), "hipEventRecord");
-    ARDIT_HIP(launch_attention_fp8(st, a8, hd, sparse), "FP8 attention launch");
-    if (e0 && e1) {
-      ARDIT_HIP(hipEventRecord(e1, st), "hipEventRecord");
-      std::lock_guard<std::mutex> g(tm.mu);
-      tm.rec.emplace_back(e0, e1);
-    }
+    ARDIT_TIMED(kTimeAttn, launch_attention_fp8(st, a8, hd, sparse), "FP8 attention launch");
   }
   return ARDIT_OK;
 }
@@ -579,21 +590,24 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   auto B16 = [](const void* p) { return static_cast<const bf16_t*>(p); };
 
   // adaLN RMSNorm #1 and the QKV projection
-  ARDIT_HIP(launch_adaln_norm(st, x, false, h, N, D, mod, mt, 0, 1, Lq, d->eps), "adaln_norm");
+  ARDIT_TIMED(kTimeElem, launch_adaln_norm(st, x, false, h, N, D, mod, mt, 0, 1, Lq, d->eps),
+              "adaln_norm");
   GemmEpiArgs e;
   e.bias = B16(w->b_qkv);
-  ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_qkv), D, qkv, 3 * D, N, 3 * D, D, e),
-            "qkv gemm");
+  ARDIT_TIMED(kTimeGemm, launch_gemm(st, kEpiBias, h, D, B16(w->w_qkv), D, qkv, 3 * D, N, 3 * D, D, e),
+              "qkv gemm");
   // QK-norm, 3D RoPE, append k~ and v to the pages
   RopeGeom rg{D, H, hd, tokens_per_frame(d), d->lat_w, kv->max_frames, kv->n_pages, d->eps,
               d->rope_theta};
-  ARDIT_HIP(launch_qk_norm_rope(st, qkv, N, rg, B16(w->g_q), B16(w->g_k), q,
-                                static_cast<bf16_t*>(kv->k_pages), kv->page_table, rs),
-            "qk_norm_rope");
-  ARDIT_HIP(launch_v_transpose(st, qkv, 3 * D, 2 * D, N, D, H, hd,
-                               static_cast<bf16_t*>(kv->v_pages), true, tokens_per_frame(d),
-                               kv->page_table, kv->max_frames, kv->n_pages, rs),
-            "v_append");
+  ARDIT_TIMED(kTimeElem,
+              launch_qk_norm_rope(st, qkv, N, rg, B16(w->g_q), B16(w->g_k), q,
+                                  static_cast<bf16_t*>(kv->k_pages), kv->page_table, rs),
+              "qk_norm_rope");
+  ARDIT_TIMED(kTimeElem,
+              launch_v_transpose(st, qkv, 3 * D, 2 * D, N, D, H, hd,
+                                 static_cast<bf16_t*>(kv->v_pages), true, tokens_per_frame(d),
+                                 kv->page_table, kv->max_frames, kv->n_pages, rs),
+              "v_append");
   if (kv_only) return ARDIT_OK;
   // self-attention over [cache | chunk]
   ARDIT_TRY(self_attention(st, d, b, q, kv, o, ws, L));
@@ -608,13 +622,17 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.dim = D;
   e.rows_per_stream = Lq;
   e.out_f32 = true;
-  ARDIT_HIP(launch_gemm(st, kEpiBiasGateRes, o, D, B16(w->w_o), D, x1, D, N, D, D, e), "o gemm");
+  ARDIT_TIMED(kTimeGemm, launch_gemm(st, kEpiBiasGateRes, o, D, B16(w->w_o), D, x1, D, N, D, D, e),
+              "o gemm");
   // cross-attention query: rms(rms(x1) g_n3 W_cq^T + b_cq) g_cq
-  ARDIT_HIP(launch_rms_gain(st, x1, true, h, N, D, B16(w->g_n3), d->eps), "cross pre-norm");
+  ARDIT_TIMED(kTimeElem, launch_rms_gain(st, x1, true, h, N, D, B16(w->g_n3), d->eps),
+              "cross pre-norm");
   e = GemmEpiArgs();
   e.bias = B16(w->b_cq);
-  ARDIT_HIP(launch_gemm(st, kEpiBias, h, D, B16(w->w_cq), D, q, D, N, D, D, e), "cq gemm");
-  ARDIT_HIP(launch_rms_gain(st, q, false, q, N, D, B16(w->g_cq), d->eps), "cross q-norm");
+  ARDIT_TIMED(kTimeGemm, launch_gemm(st, kEpiBias, h, D, B16(w->w_cq), D, q, D, N, D, D, e),
+              "cq gemm");
+  ARDIT_TIMED(kTimeElem, launch_rms_gain(st, q, false, q, N, D, B16(w->g_cq), d->eps),
+              "cross q-norm");
   const AttnArgs ca = cross_attn_args(d, b, q, ctx_k, ctx_v, o, at<float>(ws, L.attn));
   ARDIT_HIP(launch_attention(st, ca, hd, false), "cross-attention");
   // x2 = x1 + o_c W_co^T + b_co
@@ -624,12 +642,15 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.ldr = D;
   e.res_f32 = true;
   e.out_f32 = true;
-  ARDIT_HIP(launch_gemm(st, kEpiBiasRes, o, D, B16(w->w_co), D, x2, D, N, D, D, e), "co gemm");
+  ARDIT_TIMED(kTimeGemm, launch_gemm(st, kEpiBiasRes, o, D, B16(w->w_co), D, x2, D, N, D, D, e),
+              "co gemm");
   // FFN: out = x2 + gate2 * (GELU(adaLN2(x2) W_1^T + b_1) W_2^T + b_2)
-  ARDIT_HIP(launch_adaln_norm(st, x2, true, h, N, D, mod, mt, 3, 4, Lq, d->eps), "adaln_norm 2");
+  ARDIT_TIMED(kTimeElem, launch_adaln_norm(st, x2, true, h, N, D, mod, mt, 3, 4, Lq, d->eps),
+              "adaln_norm 2");
   e = GemmEpiArgs();
   e.bias = B16(w->b_1);
-  ARDIT_HIP(launch_gemm(st, kEpiBiasGelu, h, D, B16(w->w_1), D, u, F, N, F, D, e), "ffn up");
+  ARDIT_TIMED(kTimeGemm, launch_gemm(st, kEpiBiasGelu, h, D, B16(w->w_1), D, u, F, N, F, D, e),
+              "ffn up");
   e = GemmEpiArgs();
   e.bias = B16(w->b_2);
   e.res = x2;
@@ -640,7 +661,8 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   e.gate_row = 5;
   e.dim = D;
   e.rows_per_stream = Lq;
-  ARDIT_HIP(launch_gemm(st, kEpiBiasGateRes, u, F, B16(w->w_2), F, y, D, N, D, F, e), "ffn down");
+  ARDIT_TIMED(kTimeGemm, launch_gemm(st, kEpiBiasGateRes, u, F, B16(w->w_2), F, y, D, N, D, F, e),
+              "ffn down");
   return ARDIT_OK;
 }
 
@@ -1041,33 +1063,45 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
 }
 
 int ardit_timing_enable(int enable) {
+  if (enable < 0 || enable >= (1 << kTimeKinds))
+    return fail(ARDIT_EINVAL, "timing mask %d outside [0, %d]", enable, (1 << kTimeKinds) - 1);
   Timing& t = timing();
   std::lock_guard<std::mutex> g(t.mu);
-  t.enabled = enable != 0;
+  t.mask = static_cast<unsigned>(enable);
   return ARDIT_OK;
 }
 
-int ardit_timing_collect(int32_t* launches, double* total_ms) {
+int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms) {
   if (!launches || !total_ms) return fail(ARDIT_EINVAL, "outputs must be non-NULL");
+  if (kind < 0 || kind >= kTimeKinds) return fail(ARDIT_EINVAL, "timing kind %d", kind);
   Timing& t = timing();
   std::lock_guard<std::mutex> g(t.mu);
   double sum = 0.0;
   int n = 0;
   int status = ARDIT_OK;
-  for (auto& pr : t.rec) {
+  std::vector<TimedRec> keep;
+  for (auto& r : t.rec) {
+    if (r.kind != kind) {
+      keep.push_back(r);
+      continue;
+    }
     float ms = 0.f;
-    hipError_t e = hipEventSynchronize(pr.second);
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
+    hipError_t e = hipEventSynchronize(r.e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.e0, r.e1);
     if (e != hipSuccess && status == ARDIT_OK) status = hip_fail(e, "timing events");
     sum += ms;
     ++n;
-    t.pool.push_back(pr.first);
-    t.pool.push_back(pr.second);
+    t.pool.push_back(r.e0);
+    t.pool.push_back(r.e1);
   }
-  t.rec.clear();
+  t.rec.swap(keep);
   *launches = n;
   *total_ms = sum;
   return status;
+}
+
+int ardit_timing_collect(int32_t* launches, double* total_ms) {
+  return ardit_timing_collect_kind(kTimeAttn, launches, total_ms);
 }
 
 }  // extern "C"

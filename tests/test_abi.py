@@ -304,3 +304,15 @@ def test_workspace_holds_generation_buffers():
     one = A.ardit_workspace_size(d, A.Batch([192], [384], [6], [32]))
     two = A.ardit_workspace_size(d, A.Batch([192] * 2, [384] * 2, [6] * 2, [32] * 2))
     assert two - one >= 2 * 192 * 256 * 2 + 6 * 256 * 4
+
+
+def test_timing_masks_and_kinds():
+    """Host-side checks of the timing facility (no launch is recorded here)."""
+    assert _status(A.ardit_timing_enable, 8) == -1
+    assert _status(A.ardit_timing_enable, -1) == -1
+    assert _status(A.ardit_timing_collect_kind, 3) == -1
+    A.ardit_timing_enable(7)
+    A.ardit_timing_enable(False)
+    for k in (A.TIME_ATTENTION, A.TIME_GEMM, A.TIME_ELEMENTWISE):
+        assert A.ardit_timing_collect_kind(k) == (0, 0.0)
+    assert A.ardit_timing_collect() == (0, 0.0)
