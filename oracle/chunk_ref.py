@@ -70,7 +70,7 @@ def window_page_table(c: int, sink: int, window: int, frames: int):
 
 
 def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv, ws: list, shape,
-                   store=None):
+                   store=None, rho: float = 0.0, fp8: bool = False):
     """One chunk of one stream through an L-layer stack.
 
     x_init: [L_q, D] starting noise; noise: fresh noise of the steps after the
@@ -80,7 +80,8 @@ def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv,
     implementation stores a tensor between operations (each layer's output,
     the sampler's result, the committed keys and values); None keeps float64
     throughout.  Returns (x0, committed per-layer (k, v) of the chunk, the
-    per-step inputs x_tau)."""
+    per-step inputs x_tau).  rho and fp8 are the stream's attention knobs,
+    applied in every pass as block_forward applies them."""
     keep = (lambda a: a) if store is None else (lambda a: np.asarray(store(a), np.float64))
     x = np.asarray(x_init, np.float64)
     xs = []
@@ -91,7 +92,7 @@ def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv,
         for layer, w in enumerate(ws):
             ck, cv = caches[layer]
             h = keep(block_forward(h, ck, cv, frame_pos0, m_t, ctx_kv[layer][0], ctx_kv[layer][1],
-                                   w, shape)["out"])
+                                   w, shape, rho=rho, fp8=fp8)["out"])
         nxt = ts[s + 1] if s + 1 < len(ts) else None
         x = keep(sampler_step(x, h, t, nxt, noise[s] if nxt is not None else None))
     x0 = x
@@ -100,7 +101,8 @@ def generate_chunk(x_init, noise, ts, caches, frame_pos0: int, tw: dict, ctx_kv,
     h = x0
     for layer, w in enumerate(ws):
         ck, cv = caches[layer]
-        r = block_forward(h, ck, cv, frame_pos0, m0, ctx_kv[layer][0], ctx_kv[layer][1], w, shape)
+        r = block_forward(h, ck, cv, frame_pos0, m0, ctx_kv[layer][0], ctx_kv[layer][1], w, shape,
+                          rho=rho, fp8=fp8)
         committed.append((keep(r["k_new"]), keep(r["v_new"])))
         h = keep(r["out"])
     return x0, committed, xs

@@ -72,17 +72,18 @@ def _sampler_bits(x, v, tau, tau_next, eps):
 class Model:
     """Tiny-shape stack of n_layers with per-stream text K/V, on the device."""
 
-    def __init__(self, A, seed, n_layers, ctx_lens):
+    def __init__(self, A, seed, n_layers, ctx_lens, shape=SH):
         import torch
         self.A = A
+        self.shape = shape
         rng = make_rng(seed)
         self.rng = rng
         self.n_layers = n_layers
-        self.time_w = draw_time_weights(rng, SH.dim, SH.time_freq_dim)
-        self.block_w = [draw_block_weights(rng, SH) for _ in range(n_layers)]
-        self.ctx = [normal_bf16(rng, (n, SH.dim)) for n in ctx_lens]
+        self.time_w = draw_time_weights(rng, shape.dim, shape.time_freq_dim)
+        self.block_w = [draw_block_weights(rng, shape) for _ in range(n_layers)]
+        self.ctx = [normal_bf16(rng, (n, shape.dim)) for n in ctx_lens]
         self.ctx_lens = list(ctx_lens)
-        self.dims = A.dims_from_shape(SH)
+        self.dims = A.dims_from_shape(shape)
         self.tw_dev = {k: dev_bf16(v) for k, v in self.time_w.items()}
         self.tw = A.time_weights(self.tw_dev)
         self.w_dev = [upload_block_weights(w) for w in self.block_w]
@@ -91,14 +92,14 @@ class Model:
         ws_bytes = A.ardit_workspace_size(self.dims, cb)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         ctx_dev = dev_bf16(np.concatenate(self.ctx))
-        n = sum(ctx_lens) * SH.dim
+        n = sum(ctx_lens) * shape.dim
         self.ctx_k = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(n_layers)]
         self.ctx_v = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(n_layers)]
         for l in range(n_layers):
             A.ardit_ctx_kv(None, self.dims, cb, ctx_dev, self.w[l], self.ctx_k[l], self.ctx_v[l],
                            ws, ws_bytes)
         # oracle text K/V per stream and layer
-        self.ctx_ref = [[O.context_kv(c, self.block_w[l], SH.eps) for l in range(n_layers)]
+        self.ctx_ref = [[O.context_kv(c, self.block_w[l], shape.eps) for l in range(n_layers)]
                         for c in self.ctx]
 
     def workspace(self, batch):
@@ -346,3 +347,63 @@ def test_controller_drives_batched_generation(A):
                                                                              SH.head_dim)
             print(parity(k_got, kv_ref[l][0], f"stream {b} layer {l} committed k",
                          quantum=kv_ref[l][0], half_ulps=k_ulps))
+
+
+def test_chunk_generate_fp8_stream_tracks_oracle(A):
+    """A stream with FP8 self-attention (the quantisation knob) and a bf16 one
+    generate one chunk each in one call (head_dim 128, the FP8 kernel's);
+    each tracks its float64 oracle run with the same knob.  The FP8 stream is
+    held to 6e-2 of the RMS for the max error, as the FP8 block test: both
+    sides quantise their own bf16 roundings of q, k and v, so an E4M3 code can
+    differ by one step (2^-4 relative) where the two roundings straddle a
+    rounding boundary; the cosine keeps 0.9995."""
+    import torch
+    from workloads import BlockShape
+    sh = BlockShape(dim=256, n_heads=2, head_dim=128, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    lq = sh.chunk_tokens
+    n_layers = 2
+    m = Model(A, 93, n_layers, [24, 24], shape=sh)
+    rng = m.rng
+    B = 2
+    steps = [[1000.0, 500.0], [1000.0, 500.0]]
+    quant = [A.QUANT_FP8, A.QUANT_BF16]
+    cache = lq                                            # one earlier chunk each
+    ids = [list(range(0, 2 * sh.frames)), list(range(2 * sh.frames, 4 * sh.frames))]
+    pools = [PagedCache(sh, ids, 4 * sh.frames) for _ in range(n_layers)]
+    caches = [[None] * n_layers for _ in range(B)]
+    for l, p in enumerate(pools):
+        for b in range(B):
+            k = normal_bf16(rng, (cache, sh.n_heads, sh.head_dim))
+            v = normal_bf16(rng, (cache, sh.n_heads, sh.head_dim))
+            p.fill_stream(b, k, v)
+            caches[b][l] = (k, v)
+        p.upload()
+    batch = A.Batch([lq] * B, [cache] * B, [sh.frames] * B, m.ctx_lens, quant=quant)
+    ws, ws_bytes = m.workspace(batch)
+    x_init = [normal_bf16(rng, (lq, sh.dim)) for _ in range(B)]
+    noise = [[normal_bf16(rng, (lq, sh.dim))] for _ in range(B)]
+    x0 = torch.empty((B * lq, sh.dim), dtype=torch.bfloat16, device="cuda")
+    A.ardit_chunk_generate(None, m.dims, batch, [2, 2], steps, dev_bf16(np.concatenate(x_init)),
+                           dev_bf16(np.concatenate([n[0] for n in noise])[None]),
+                           [p.kv(A) for p in pools], m.tw, m.ctx_k, m.ctx_v, m.w, x0, ws,
+                           ws_bytes)
+    _sync()
+    got = host_f32(x0)
+    for b in range(B):
+        fp8 = quant[b] == A.QUANT_FP8
+        x0_ref, kv_ref, xs_ref = O.chunk_ref.generate_chunk(
+            x_init[b], noise[b], steps[b], caches[b], sh.frames, m.time_w, m.ctx_ref[b],
+            m.block_w, sh, store=bf16_round, fp8=fp8)
+        tau = steps[b][-1] / 1000.0
+        v_last = (xs_ref[-1] - x0_ref) / tau
+        k_ulps = 2.0 * np.sqrt(n_layers * 3 * 2)
+        print(parity(got[b * lq:(b + 1) * lq], x0_ref, f"{'FP8' if fp8 else 'bf16'} stream x0",
+                     tol=6e-2 if fp8 else 2e-2,
+                     quantum=np.abs(xs_ref[-1]) + tau * np.abs(v_last), half_ulps=k_ulps))
+        own = ids[b][cache // sh.tokens_per_frame:]
+        for l, p in enumerate(pools):
+            kb, vb = p.device_bits()
+            k_got = np.transpose(bits_to_f32(kb[own]), (0, 2, 1, 3)).reshape(lq, sh.n_heads,
+                                                                             sh.head_dim)
+            print(parity(k_got, kv_ref[l][0], f"{'FP8' if fp8 else 'bf16'} layer {l} committed k",
+                         tol=6e-2 if fp8 else 2e-2, quantum=kv_ref[l][0], half_ulps=k_ulps))
