@@ -96,8 +96,9 @@ typedef struct {
  * the packed activations. */
 typedef struct {
   int32_t n_streams;          /* 1 .. ARDIT_MAX_STREAMS */
-  const int32_t* q_lens;      /* chunk tokens per stream; block calls: frames_per_chunk * T each */
-  const int32_t* cache_lens;  /* tokens already in the stream's cache; a multiple of T */
+  const int32_t* q_lens;      /* chunk tokens per stream (<= 2^22 in all); block calls:
+                                 frames_per_chunk * T each */
+  const int32_t* cache_lens;  /* tokens already in the stream's cache; a multiple of T, <= 2^30 */
   const int32_t* frame_pos0;  /* absolute latent-frame index of the chunk's first frame (RoPE t) */
   const int32_t* ctx_lens;    /* text tokens per stream (>= 1) */
   const float* sparsity;      /* attention sparsity rho per stream in [0, 1], or NULL for all 0

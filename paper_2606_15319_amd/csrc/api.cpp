@@ -103,6 +103,8 @@ int check_batch(const ardit_dims* d, const ardit_batch* b, unsigned use) {
       if (c < 0 || c % T != 0)
         return fail(ARDIT_ESHAPE, "cache_lens[%d] = %d is not a non-negative multiple of %d", i,
                     c, T);
+      // with at most 2^22 queries, cache + chunk stays below 2^31 keys
+      if (c > (1 << 30)) return fail(ARDIT_ECAPACITY, "cache_lens[%d] = %d above 2^30", i, c);
     }
     if ((use & kUsePos) && b->frame_pos0[i] < 0)
       return fail(ARDIT_EINVAL, "frame_pos0[%d] = %d is negative", i, b->frame_pos0[i]);
@@ -165,7 +167,7 @@ SparseBytes sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b) {
     for (int i = 0; i < b->n_streams; ++i) {
       N += b->q_lens[i];
       if (b->quant[i] == ARDIT_QUANT_FP8 && b->q_lens[i] > 0)
-        keys += kAttnKTile * ceil_div(b->cache_lens[i] + b->q_lens[i], kAttnKTile);
+        keys += kAttnKTile * ceil_div(static_cast<int64_t>(b->cache_lens[i]) + b->q_lens[i], kAttnKTile);
     }
     const size_t qb = static_cast<size_t>(N) * d->dim;
     z.f8q = up(qb) + up(qb / 32);
@@ -745,6 +747,7 @@ int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_
   if (!bytes) return fail(ARDIT_EINVAL, "bytes is NULL");
   ARDIT_TRY(check_batch(dims, batch, 0));
   if (batch->q_lens) ARDIT_TRY(check_batch(dims, batch, kUseQ));
+  if (batch->cache_lens) ARDIT_TRY(check_batch(dims, batch, kUseCache));
   if (batch->ctx_lens) ARDIT_TRY(check_batch(dims, batch, kUseCtx));
   if (batch_sparse(batch)) {
     if (!batch->q_lens || !batch->cache_lens)

@@ -114,6 +114,13 @@ def test_too_many_streams():
     assert _status(A.ardit_workspace_size, d, b) == -1
 
 
+def test_cache_beyond_2_30_rejected():
+    d = _dims()
+    T = d.lat_h * d.lat_w
+    assert _status(A.ardit_workspace_size, d, A.Batch([100], [(1 << 30) + T])) == -3
+    assert A.ardit_workspace_size(d, A.Batch([100], [1 << 30])) > 0
+
+
 def test_attn_fwd_validation():
     d = _dims()
     b = A.Batch([100], [64])
