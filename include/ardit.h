@@ -76,7 +76,8 @@ typedef enum {
   ARDIT_ECAPACITY = -3,   /* a stream's keys exceed its page table or a length is out of range */
   ARDIT_EWORKSPACE = -4,  /* workspace smaller than ardit_workspace_size reports */
   ARDIT_EUNSUPPORTED = -5,/* shape outside what the kernels support (see above) */
-  ARDIT_EHIP = -6         /* the HIP runtime reported an error */
+  ARDIT_EHIP = -6,        /* the HIP runtime reported an error */
+  ARDIT_EHOST = -7        /* host memory ran out inside the call */
 } ardit_status;
 
 /* Model and chunk geometry (host struct). */

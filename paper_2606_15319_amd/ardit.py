@@ -30,7 +30,8 @@ _lib = C.CDLL(LIB_PATH)
 ARDIT_MAX_STREAMS = 64
 ARDIT_MAX_STEPS = 16
 STATUS = {0: "ARDIT_OK", -1: "ARDIT_EINVAL", -2: "ARDIT_ESHAPE", -3: "ARDIT_ECAPACITY",
-          -4: "ARDIT_EWORKSPACE", -5: "ARDIT_EUNSUPPORTED", -6: "ARDIT_EHIP"}
+          -4: "ARDIT_EWORKSPACE", -5: "ARDIT_EUNSUPPORTED", -6: "ARDIT_EHIP",
+          -7: "ARDIT_EHOST"}
 
 
 class ArditError(RuntimeError):

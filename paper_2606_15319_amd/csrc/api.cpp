@@ -18,15 +18,15 @@ using namespace ardit;
 
 namespace {
 
-thread_local std::string g_last_error;
+// a fixed buffer: recording an error never allocates, so it also works when
+// host memory has run out
+thread_local char g_last_error[512];
 
 int fail(int status, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return status;
 }
 
@@ -720,6 +720,9 @@ int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
 namespace ardit {
 // the calling thread's error detail, for the controller's translation unit
 int set_error(int status, const char* msg) { return fail(status, "%s", msg); }
+// every entry point ends here when a host-side exception (an allocation that
+// failed) would otherwise leave the library through its C interface
+int host_failure() { return fail(ARDIT_EHOST, "host memory exhausted"); }
 }  // namespace ardit
 
 // ======================================================================== ABI
@@ -734,15 +737,16 @@ const char* ardit_status_str(int s) {
     case ARDIT_EWORKSPACE: return "ARDIT_EWORKSPACE";
     case ARDIT_EUNSUPPORTED: return "ARDIT_EUNSUPPORTED";
     case ARDIT_EHIP: return "ARDIT_EHIP";
+    case ARDIT_EHOST: return "ARDIT_EHOST";
     default: return "ARDIT_UNKNOWN";
   }
 }
 
-const char* ardit_last_error(void) { return g_last_error.c_str(); }
+const char* ardit_last_error(void) { return g_last_error; }
 
 int ardit_version(void) { return 500; }
 
-int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) {
+int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) try {
   ARDIT_TRY(check_dims(dims));
   if (!bytes) return fail(ARDIT_EINVAL, "bytes is NULL");
   ARDIT_TRY(check_batch(dims, batch, 0));
@@ -758,11 +762,13 @@ int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_
   *bytes = ws_layout(dims, batch->n_streams, sum_q(batch), sum_ctx(batch),
                      sparse_ws_bytes(dims, batch)).total;
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_time_mod(hipStream_t stream, const ardit_dims* dims, int32_t n_streams,
                    const float* t_host, const ardit_time_weights* tw, float* mod_out, void* ws,
-                   size_t ws_bytes) {
+                   size_t ws_bytes) try {
   ARDIT_TRY(check_dims(dims));
   if (n_streams < 1 || n_streams > ARDIT_MAX_STREAMS)
     return fail(ARDIT_EINVAL, "n_streams %d not in [1, %d]", n_streams, ARDIT_MAX_STREAMS);
@@ -773,11 +779,13 @@ int ardit_time_mod(hipStream_t stream, const ardit_dims* dims, int32_t n_streams
   const Ws L = ws_layout(dims, n_streams, 0, 0);
   if (ws_bytes < L.h) return fail(ARDIT_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.h);
   return time_mod_chain(stream, dims, n_streams, t_host, tw, mod_out, ws, L);
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_ctx_kv(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                  const void* ctx, const ardit_block_weights* w, void* ctx_k, void* ctx_v,
-                 void* ws, size_t ws_bytes) {
+                 void* ws, size_t ws_bytes) try {
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseCtx));
   ARDIT_TRY(check_ptr(ctx, "ctx"));
@@ -808,11 +816,13 @@ int ardit_ctx_kv(hipStream_t stream, const ardit_dims* dims, const ardit_batch* 
                                static_cast<bf16_t*>(ctx_v), false, 0, nullptr, 0, 0, rs),
             "ctx v layout");
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                     const void* qkv, const void* g_q, const void* g_k, const ardit_kv_paged* kv,
-                    void* q_out) {
+                    void* q_out) try {
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache | kUsePos | kChunkQ));
   ARDIT_TRY(check_kv(dims, batch, kv));
@@ -836,10 +846,12 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
                                kv->n_pages, rs),
             "v_append");
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
-                   const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes) {
+                   const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes) try {
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
   ARDIT_TRY(check_kv(dims, batch, kv));
@@ -849,10 +861,12 @@ int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
   return self_attention(stream, dims, batch, q, kv, o, ws, L);
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_mx_quantize(hipStream_t stream, const void* x, int64_t rows, int32_t cols, int32_t ld,
-                      void* codes, void* scales) {
+                      void* codes, void* scales) try {
   if (!x || !codes || !scales) return fail(ARDIT_EINVAL, "pointers must be non-NULL");
   if (rows < 0 || cols <= 0 || cols % 32 != 0)
     return fail(ARDIT_ESHAPE, "cols %d must be a positive multiple of 32", cols);
@@ -863,11 +877,13 @@ int ardit_mx_quantize(hipStream_t stream, const void* x, int64_t rows, int32_t c
                                     static_cast<uint8_t*>(codes), static_cast<uint8_t*>(scales)),
             "mx quantisation launch");
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                         const void* q, const ardit_kv_paged* kv, int32_t* blocks,
-                        int32_t row_stride, void* ws, size_t ws_bytes) {
+                        int32_t row_stride, void* ws, size_t ws_bytes) try {
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
   ARDIT_TRY(check_kv(dims, batch, kv));
@@ -898,22 +914,26 @@ int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_
                         at<float>(ws, L.sp_scores));
   ARDIT_HIP(launch_sparse_select(stream, a, dims->head_dim), "block selection launch");
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                            const void* x, const ardit_kv_paged* kv, const float* mod,
                            const void* ctx_k, const void* ctx_v, const ardit_block_weights* w,
-                           void* out, void* ws, size_t ws_bytes) {
+                           void* out, void* ws, size_t ws_bytes) try {
   ARDIT_TRY(check_block_args(dims, batch, x, kv, mod, ctx_k, ctx_v, w, out));
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
   return block_chain(stream, dims, batch, x, kv, mod, ctx_k, ctx_v, w, out, ws, L);
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x, ardit_kv_paged kv,
                     int32_t cache_len, int32_t frame_pos0, const float* mod, const void* ctx_k,
                     const void* ctx_v, int32_t ctx_len, const ardit_block_weights* w, void* out,
-                    void* ws, size_t ws_bytes) {
+                    void* ws, size_t ws_bytes) try {
   ARDIT_TRY(check_dims(dims));
   const int32_t q_len = chunk_tokens(dims);
   ardit_batch b;
@@ -926,12 +946,14 @@ int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x, a
   b.quant = nullptr;
   return ardit_block_fwd_varlen(stream, dims, &b, x, &kv, mod, ctx_k, ctx_v, w, out, ws,
                                 ws_bytes);
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                     int32_t n_layers, const void* x, const ardit_kv_paged* kv, const float* mod,
                     const void* const* ctx_k, const void* const* ctx_v,
-                    const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes) {
+                    const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes) try {
   if (n_layers < 1) return fail(ARDIT_EINVAL, "n_layers %d must be >= 1", n_layers);
   if (!kv || !ctx_k || !ctx_v || !w) return fail(ARDIT_EINVAL, "per-layer arrays must be non-NULL");
   for (int l = 0; l < n_layers; ++l)
@@ -945,11 +967,13 @@ int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batc
     ARDIT_TRY(block_chain(stream, dims, batch, l == 0 ? x : out, &kv[l], mod, ctx_k[l], ctx_v[l],
                           &w[l], out, ws, L));
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_window_pages(int32_t chunk, int32_t sink, int32_t window, int32_t frames_per_chunk,
                        int32_t page_base, int32_t* table, int32_t max_frames,
-                       int32_t* cache_frames) {
+                       int32_t* cache_frames) try {
   if (chunk < 0 || sink < 0 || window < 0 || frames_per_chunk < 1 || page_base < 0)
     return fail(ARDIT_EINVAL, "chunk %d, sink %d, window %d, page_base %d must be >= 0 and "
                 "frames_per_chunk %d >= 1", chunk, sink, window, page_base, frames_per_chunk);
@@ -977,6 +1001,8 @@ int ardit_window_pages(int32_t chunk, int32_t sink, int32_t window, int32_t fram
   put(chunk);
   *cache_frames = static_cast<int32_t>(held * frames_per_chunk);
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
@@ -984,7 +1010,7 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
                          int32_t t_ld, const void* x_init, const void* noise,
                          const ardit_kv_paged* kv, const ardit_time_weights* tw,
                          const void* const* ctx_k, const void* const* ctx_v,
-                         const ardit_block_weights* w, void* x0_out, void* ws, size_t ws_bytes) {
+                         const ardit_block_weights* w, void* x0_out, void* ws, size_t ws_bytes) try {
   ARDIT_TRY(check_dims(dims));
   ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache | kUsePos | kUseCtx | kChunkQ));
   if (n_layers < 1) return fail(ARDIT_EINVAL, "n_layers %d must be >= 1", n_layers);
@@ -1063,18 +1089,22 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
     }
   }
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int ardit_timing_enable(int enable) {
+int ardit_timing_enable(int enable) try {
   if (enable < 0 || enable >= (1 << kTimeKinds))
     return fail(ARDIT_EINVAL, "timing mask %d outside [0, %d]", enable, (1 << kTimeKinds) - 1);
   Timing& t = timing();
   std::lock_guard<std::mutex> g(t.mu);
   t.mask = static_cast<unsigned>(enable);
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms) {
+int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms) try {
   if (!launches || !total_ms) return fail(ARDIT_EINVAL, "outputs must be non-NULL");
   if (kind < 0 || kind >= kTimeKinds) return fail(ARDIT_EINVAL, "timing kind %d", kind);
   Timing& t = timing();
@@ -1101,10 +1131,14 @@ int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms)
   *launches = n;
   *total_ms = sum;
   return status;
+} catch (...) {
+  return host_failure();
 }
 
-int ardit_timing_collect(int32_t* launches, double* total_ms) {
+int ardit_timing_collect(int32_t* launches, double* total_ms) try {
   return ardit_timing_collect_kind(kTimeAttn, launches, total_ms);
+} catch (...) {
+  return host_failure();
 }
 
 }  // extern "C"

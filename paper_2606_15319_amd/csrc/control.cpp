@@ -14,10 +14,12 @@
 namespace ardit {
 // error reporting shared with the rest of the library (api.cpp)
 int set_error(int status, const char* msg);
+int host_failure();
 }  // namespace ardit
 
 namespace {
 
+using ardit::host_failure;
 using ardit::set_error;
 
 bool is_fin(double x) { return std::isfinite(x); }
@@ -70,7 +72,7 @@ int check_frontier(int32_t n_cfgs, const ardit_fidelity* cfgs, int32_t nf, const
 extern "C" {
 
 int ardit_pareto_frontier(int32_t n, const ardit_fidelity* cfgs, int32_t* frontier,
-                          int32_t* n_frontier, double* q_floor) {
+                          int32_t* n_frontier, double* q_floor) try {
   if (n < 1 || !cfgs || !frontier || !n_frontier || !q_floor)
     return set_error(ARDIT_EINVAL, "pareto_frontier: empty set or NULL pointer");
   for (int i = 0; i < n; ++i)
@@ -103,11 +105,13 @@ int ardit_pareto_frontier(int32_t n, const ardit_fidelity* cfgs, int32_t* fronti
   *q_floor = (n % 2) ? q[n / 2] : 0.5 * (q[n / 2 - 1] + q[n / 2]);
   *n_frontier = m;
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_bmpr_select(int32_t n_cfgs, const ardit_fidelity* cfgs, int32_t n_frontier,
                       const int32_t* frontier, double q_floor, double budget_ms, int32_t* cfg,
-                      int32_t* mode) {
+                      int32_t* mode) try {
   int s = check_frontier(n_cfgs, cfgs, n_frontier, frontier);
   if (s != ARDIT_OK) return s;
   if (!cfg || !mode) return set_error(ARDIT_EINVAL, "bmpr_select: NULL output");
@@ -119,12 +123,14 @@ int ardit_bmpr_select(int32_t n_cfgs, const ardit_fidelity* cfgs, int32_t n_fron
   *cfg = c;
   *mode = md;
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_control_tick(const ardit_ctl_params* p, int32_t n_cfgs, const ardit_fidelity* cfgs,
                        int32_t n_frontier, const int32_t* frontier, double q_floor,
                        int32_t n_streams, const ardit_stream_state* st,
-                       ardit_stream_decision* out) {
+                       ardit_stream_decision* out) try {
   if (!p || !st || !out || n_streams < 0) return set_error(ARDIT_EINVAL, "control_tick: NULL argument");
   int s = check_frontier(n_cfgs, cfgs, n_frontier, frontier);
   if (s != ARDIT_OK) return s;
@@ -235,11 +241,13 @@ int ardit_control_tick(const ardit_ctl_params* p, int32_t n_cfgs, const ardit_fi
   }
   std::copy(d.begin(), d.end(), out);
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_evict_for(int32_t n, const double* credits, const int32_t* resident_pages,
                     int32_t requester, int64_t free_pages, int64_t need_pages, int32_t* evict,
-                    int32_t* n_evict) {
+                    int32_t* n_evict) try {
   if (n < 0 || (n > 0 && (!credits || !resident_pages)) || !evict || !n_evict)
     return set_error(ARDIT_EINVAL, "evict_for: NULL argument");
   for (int i = 0; i < n; ++i)
@@ -265,10 +273,12 @@ int ardit_evict_for(int32_t n, const double* credits, const int32_t* resident_pa
   std::copy(chosen.begin(), chosen.end(), evict);
   *n_evict = m;
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int ardit_admit(int32_t n_workers, const int32_t* streams_per_worker, double first_chunk_ms,
-                int32_t* home, double* slack_ms) {
+                int32_t* home, double* slack_ms) try {
   if (n_workers < 1 || !streams_per_worker || !home || !slack_ms || !is_fin(first_chunk_ms))
     return set_error(ARDIT_EINVAL, "admit: malformed argument");
   int best = 0;
@@ -277,6 +287,8 @@ int ardit_admit(int32_t n_workers, const int32_t* streams_per_worker, double fir
   *home = best;
   *slack_ms = 4.0 * first_chunk_ms;
   return ARDIT_OK;
+} catch (...) {
+  return host_failure();
 }
 
 }  // extern "C"
