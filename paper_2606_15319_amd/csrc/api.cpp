@@ -410,7 +410,23 @@ struct TimedLaunch {
     Timing& tm = timing();
     std::lock_guard<std::mutex> g(tm.mu);
     tm.rec.push_back(TimedRec{kind, e0, e1});
+    e0 = e1 = nullptr;
     return e;
+  }
+  // events not handed to the record (a failed launch, or only one event
+  // created) go back to the pool
+  ~TimedLaunch() {
+    if (!e0 && !e1) return;
+    Timing& tm = timing();
+    std::lock_guard<std::mutex> g(tm.mu);
+    for (hipEvent_t e : {e0, e1}) {
+      if (!e) continue;
+      try {
+        tm.pool.push_back(e);
+      } catch (...) {
+        (void)hipEventDestroy(e);
+      }
+    }
   }
 };
 
