@@ -28,7 +28,9 @@ __device__ __forceinline__ void load8(const float* p, float* f) {
 
 // A workgroup of 4 waves handles kRowsPerGroup consecutive rows, 2 per wave;
 // the per-row vectors it shares (modulation, gains) are staged once in LDS as
-// fp32.  A lane holds chunks lane + 64 i (i < MAXC) of 8 elements of each of
+// fp32, the first four of each 8-element chunk in one array and the last four
+// in a second, so a wave's 16-byte reads are consecutive (pairs of 16-byte
+// reads 32 bytes apart made two-way bank conflicts).  A lane holds chunks lane + 64 i (i < MAXC) of 8 elements of each of
 // its rows, so every row is read from HBM once and all its loads are in
 // flight together.
 constexpr int kRowsPerGroup = 8;
@@ -42,7 +44,7 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
     const T* __restrict__ x, bf16_t* __restrict__ out, int N, int D,
     const float* __restrict__ mod, const float* __restrict__ mod_table, int shift_row,
     int scale_row, int rows_per_stream, float eps) {
-  extern __shared__ float4 lds_mod[];   // D / 4 of (1 + scale), then D / 4 of shift
+  extern __shared__ float4 lds_mod[];   // D / 4 of (1 + scale), then D / 4 of shift (split halves)
   const int lane = threadIdx.x & 63;
   const int row0 = blockIdx.x * kRowsPerGroup + (threadIdx.x >> 6) * kRowsPerWave;
   const int nchunk = D >> 3;
@@ -65,8 +67,9 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
     const float4* tsc = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(scale_row) * D);
     for (int k = threadIdx.x; k < D / 4; k += 256) {
       const float4 a = msc[k], c = tsc[k], sh = msh[k], th = tsh[k];
-      lds_mod[k] = make_float4(1.f + a.x + c.x, 1.f + a.y + c.y, 1.f + a.z + c.z, 1.f + a.w + c.w);
-      lds_mod[D / 4 + k] = make_float4(sh.x + th.x, sh.y + th.y, sh.z + th.z, sh.w + th.w);
+      const int at = (k & 1) * (D / 8) + (k >> 1);   // half k % 2 of chunk k / 2
+      lds_mod[at] = make_float4(1.f + a.x + c.x, 1.f + a.y + c.y, 1.f + a.z + c.z, 1.f + a.w + c.w);
+      lds_mod[D / 4 + at] = make_float4(sh.x + th.x, sh.y + th.y, sh.z + th.z, sh.w + th.w);
     }
   }
   __syncthreads();
@@ -87,8 +90,8 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
     for (int i = 0; i < MAXC; ++i) {
       const int c = lane + 64 * i;
       if (c < nchunk) {
-        const float4 a0 = lds_mod[2 * c], a1 = lds_mod[2 * c + 1];
-        const float4 b0 = lds_mod[D / 4 + 2 * c], b1 = lds_mod[D / 4 + 2 * c + 1];
+        const float4 a0 = lds_mod[c], a1 = lds_mod[nchunk + c];
+        const float4 b0 = lds_mod[D / 4 + c], b1 = lds_mod[D / 4 + nchunk + c];
         const float sa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
         const float sb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
         float y[8];
@@ -122,8 +125,8 @@ __global__ __launch_bounds__(256) void rms_gain_kernel(const T* in, bf16_t* out,
   for (int k = threadIdx.x; k < D / 8; k += 256) {
     float g[8];
     load8(gain + 8 * k, g);
-    lds_gain[2 * k] = make_float4(g[0], g[1], g[2], g[3]);
-    lds_gain[2 * k + 1] = make_float4(g[4], g[5], g[6], g[7]);
+    lds_gain[k] = make_float4(g[0], g[1], g[2], g[3]);
+    lds_gain[D / 8 + k] = make_float4(g[4], g[5], g[6], g[7]);
   }
   __syncthreads();
 #pragma unroll
@@ -143,7 +146,7 @@ __global__ __launch_bounds__(256) void rms_gain_kernel(const T* in, bf16_t* out,
     for (int i = 0; i < MAXC; ++i) {
       const int c = lane + 64 * i;
       if (c < nchunk) {
-        const float4 g0 = lds_gain[2 * c], g1 = lds_gain[2 * c + 1];
+        const float4 g0 = lds_gain[c], g1 = lds_gain[nchunk + c];
         const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
         float y[8];
 #pragma unroll
@@ -274,11 +277,11 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p)
   for (int k = threadIdx.x; k < p.D / 8; k += 256) {
     float g[8];
     unpack8(reinterpret_cast<const uint4*>(p.g_q)[k], g);
-    lg_q[2 * k] = make_float4(g[0], g[1], g[2], g[3]);
-    lg_q[2 * k + 1] = make_float4(g[4], g[5], g[6], g[7]);
+    lg_q[k] = make_float4(g[0], g[1], g[2], g[3]);
+    lg_q[p.D / 8 + k] = make_float4(g[4], g[5], g[6], g[7]);
     unpack8(reinterpret_cast<const uint4*>(p.g_k)[k], g);
-    lg_k[2 * k] = make_float4(g[0], g[1], g[2], g[3]);
-    lg_k[2 * k + 1] = make_float4(g[4], g[5], g[6], g[7]);
+    lg_k[k] = make_float4(g[0], g[1], g[2], g[3]);
+    lg_k[p.D / 8 + k] = make_float4(g[4], g[5], g[6], g[7]);
   }
   // rotation of pair `lane` of a head for each of this wave's rows
 #pragma unroll
@@ -342,7 +345,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p)
         const float4 sv = *reinterpret_cast<const float4*>(rsn + (e0 >> 1));
         const float cc[4] = {cv.x, cv.y, cv.z, cv.w}, ss[4] = {sv.x, sv.y, sv.z, sv.w};
         float a[8], y[8];
-        const float4 g0 = lg_q[2 * c], g1 = lg_q[2 * c + 1];
+        const float4 g0 = lg_q[c], g1 = lg_q[nchunk + c];
         const float gq[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
         unpack8(qraw[r][i], a);
 #pragma unroll
@@ -352,7 +355,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p)
           y[2 * e + 1] = x0 * ss[e] + x1 * cc[e];
         }
         qo[c] = pack8(y);
-        const float4 k0 = lg_k[2 * c], k1 = lg_k[2 * c + 1];
+        const float4 k0 = lg_k[c], k1 = lg_k[nchunk + c];
         const float gk[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
         unpack8(kraw[r][i], a);
 #pragma unroll
