@@ -65,11 +65,16 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
     const float4* msc = reinterpret_cast<const float4*>(mod + (static_cast<size_t>(b) * 6 + scale_row) * D);
     const float4* tsh = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(shift_row) * D);
     const float4* tsc = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(scale_row) * D);
-    for (int k = threadIdx.x; k < D / 4; k += 256) {
-      const float4 a = msc[k], c = tsc[k], sh = msh[k], th = tsh[k];
-      const int at = (k & 1) * (D / 8) + (k >> 1);   // half k % 2 of chunk k / 2
-      lds_mod[at] = make_float4(1.f + a.x + c.x, 1.f + a.y + c.y, 1.f + a.z + c.z, 1.f + a.w + c.w);
-      lds_mod[D / 4 + at] = make_float4(sh.x + th.x, sh.y + th.y, sh.z + th.z, sh.w + th.w);
+    for (int k = threadIdx.x; k < D / 8; k += 256) {   // chunk k, both halves
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const float4 a = msc[2 * k + hf], c = tsc[2 * k + hf];
+        const float4 sh = msh[2 * k + hf], th = tsh[2 * k + hf];
+        lds_mod[hf * (D / 8) + k] =
+            make_float4(1.f + a.x + c.x, 1.f + a.y + c.y, 1.f + a.z + c.z, 1.f + a.w + c.w);
+        lds_mod[D / 4 + hf * (D / 8) + k] =
+            make_float4(sh.x + th.x, sh.y + th.y, sh.z + th.z, sh.w + th.w);
+      }
     }
   }
   __syncthreads();
