@@ -618,14 +618,10 @@ int block_chain(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const
   RopeGeom rg{D, H, hd, tokens_per_frame(d), d->lat_w, kv->max_frames, kv->n_pages, d->eps,
               d->rope_theta};
   ARDIT_TIMED(kTimeElem,
-              launch_qk_norm_rope(st, qkv, N, rg, B16(w->g_q), B16(w->g_k), q,
-                                  static_cast<bf16_t*>(kv->k_pages), kv->page_table, rs),
-              "qk_norm_rope");
-  ARDIT_TIMED(kTimeElem,
-              launch_v_transpose(st, qkv, 3 * D, 2 * D, N, D, H, hd,
-                                 static_cast<bf16_t*>(kv->v_pages), true, tokens_per_frame(d),
-                                 kv->page_table, kv->max_frames, kv->n_pages, rs),
-              "v_append");
+              launch_kv_append(st, qkv, N, rg, B16(w->g_q), B16(w->g_k), q,
+                               static_cast<bf16_t*>(kv->k_pages),
+                               static_cast<bf16_t*>(kv->v_pages), kv->page_table, rs),
+              "qk_norm_rope / kv append");
   if (kv_only) return ARDIT_OK;
   // self-attention over [cache | chunk]
   ARDIT_TRY(self_attention(st, d, b, q, kv, o, ws, L));
@@ -851,16 +847,11 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
   const int D = dims->dim;
   RopeGeom rg{D, dims->n_heads, dims->head_dim, tokens_per_frame(dims), dims->lat_w,
               kv->max_frames, kv->n_pages, dims->eps, dims->rope_theta};
-  ARDIT_HIP(launch_qk_norm_rope(stream, static_cast<const bf16_t*>(qkv), N, rg,
-                                static_cast<const bf16_t*>(g_q), static_cast<const bf16_t*>(g_k),
-                                static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(kv->k_pages),
-                                kv->page_table, rs),
-            "qk_norm_rope");
-  ARDIT_HIP(launch_v_transpose(stream, static_cast<const bf16_t*>(qkv), 3 * D, 2 * D, N, D,
-                               dims->n_heads, dims->head_dim, static_cast<bf16_t*>(kv->v_pages),
-                               true, tokens_per_frame(dims), kv->page_table, kv->max_frames,
-                               kv->n_pages, rs),
-            "v_append");
+  ARDIT_HIP(launch_kv_append(stream, static_cast<const bf16_t*>(qkv), N, rg,
+                             static_cast<const bf16_t*>(g_q), static_cast<const bf16_t*>(g_k),
+                             static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(kv->k_pages),
+                             static_cast<bf16_t*>(kv->v_pages), kv->page_table, rs),
+            "qk_norm_rope / kv append");
   return ARDIT_OK;
 } catch (...) {
   return host_failure();

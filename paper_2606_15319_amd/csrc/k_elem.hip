@@ -8,6 +8,8 @@
 // a workgroup's rows (modulation, gains, rotation terms) are staged in LDS.
 #include <math.h>
 
+#include <algorithm>
+
 #include "launch.h"
 
 namespace ardit {
@@ -252,12 +254,13 @@ __device__ __forceinline__ int clamp_page(int p, int n_pages) {
 // A workgroup handles kRowsPerGroup rows, 2 per wave.  Per row, lane k < d/2
 // computes the rotation (cos, sin) of pair k, shared through LDS; the gains
 // are staged in LDS as fp32; both rows' q and k are loaded before any math.
+// lds_qk: g_q (D / 4 float4), g_k (D / 4), then cos / sin per row
 template <int MAXC>
-__global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p) {
-  extern __shared__ float4 lds_qk[];   // g_q (D / 4), g_k (D / 4), then cos / sin per row
+__device__ __forceinline__ void qk_norm_rope_group(const QkRopeParams& p, int group,
+                                                   float4* lds_qk) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int row0 = blockIdx.x * kRowsPerGroup + wave * kRowsPerWave;
+  const int row0 = group * kRowsPerGroup + wave * kRowsPerWave;
   const int nchunk = p.D >> 3;
   float4* lg_q = lds_qk;
   float4* lg_k = lds_qk + p.D / 4;
@@ -376,10 +379,15 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p)
   }
 }
 
-hipError_t launch_qk_norm_rope(hipStream_t st, const bf16_t* qkv, int N, const RopeGeom& g,
-                               const bf16_t* g_q, const bf16_t* g_k, bf16_t* q_out,
-                               bf16_t* k_pages, const int32_t* page_table, const RowStreams& rs) {
-  if (N == 0) return hipSuccess;
+template <int MAXC>
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p) {
+  extern __shared__ float4 lds_qk[];
+  qk_norm_rope_group<MAXC>(p, blockIdx.x, lds_qk);
+}
+
+static QkRopeParams qk_params(const bf16_t* qkv, int N, const RopeGeom& g, const bf16_t* g_q,
+                              const bf16_t* g_k, bf16_t* q_out, bf16_t* k_pages,
+                              const int32_t* page_table, const RowStreams& rs) {
   QkRopeParams p;
   p.qkv = qkv;
   p.q_out = q_out;
@@ -410,8 +418,20 @@ hipError_t launch_qk_norm_rope(hipStream_t st, const bf16_t* qkv, int N, const R
       p.inv_freq[pair++] =
           static_cast<float>(pow(static_cast<double>(g.theta), -2.0 * k / segs[a]));
   p.rs = rs;
+  return p;
+}
+
+static size_t qk_lds_bytes(int D) {
+  return 2 * sizeof(float) * D + 2 * sizeof(float) * kRowsPerGroup * 64;
+}
+
+hipError_t launch_qk_norm_rope(hipStream_t st, const bf16_t* qkv, int N, const RopeGeom& g,
+                               const bf16_t* g_q, const bf16_t* g_k, bf16_t* q_out,
+                               bf16_t* k_pages, const int32_t* page_table, const RowStreams& rs) {
+  if (N == 0) return hipSuccess;
+  const QkRopeParams p = qk_params(qkv, N, g, g_q, g_k, q_out, k_pages, page_table, rs);
   const dim3 grid((N + kRowsPerGroup - 1) / kRowsPerGroup);
-  const size_t lds = 2 * sizeof(float) * g.D + 2 * sizeof(float) * kRowsPerGroup * 64;
+  const size_t lds = qk_lds_bytes(g.D);
   switch (row_chunks(g.D)) {
 #define ARDIT_QK_CASE(C) \
     case C: hipLaunchKernelGGL(qk_norm_rope_kernel<C>, grid, dim3(256), lds, st, p); break;
@@ -489,10 +509,9 @@ __global__ __launch_bounds__(256) void v_transpose_kernel(const VtParams p) {
 // so each 8-token group lies in one stream and one page.
 constexpr int kVaRows = 64;
 
-__global__ __launch_bounds__(256) void v_append16_kernel(const VtParams p) {
-  __shared__ __attribute__((aligned(16))) bf16_t tile[kVaRows][128];
-  const int n0 = blockIdx.x * kVaRows;
-  const int h = blockIdx.y;
+__device__ __forceinline__ void v_append16_block(const VtParams& p, int nb, int h,
+                                                 bf16_t (*tile)[128]) {
+  const int n0 = nb * kVaRows;
   const int cpr = p.hd >> 3;  // 16-byte chunks per row of one head
   for (int c = threadIdx.x; c < kVaRows * cpr; c += 256) {
     const int r = c / cpr, cc = c - r * cpr;
@@ -532,11 +551,32 @@ __global__ __launch_bounds__(256) void v_append16_kernel(const VtParams p) {
   }
 }
 
-hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int col_off, int N,
-                              int D, int H, int hd, bf16_t* dst, bool paged, int T,
-                              const int32_t* page_table, int max_frames, int n_pages,
-                              const RowStreams& rs) {
-  if (N == 0) return hipSuccess;
+__global__ __launch_bounds__(256) void v_append16_kernel(const VtParams p) {
+  __shared__ __attribute__((aligned(16))) bf16_t tile[kVaRows][128];
+  v_append16_block(p, blockIdx.x, blockIdx.y, tile);
+}
+
+// The key path (QK-norm + RoPE + key append) and the 16-byte value append in
+// one launch: the first qk_groups workgroups take 8-row groups of q and k, the
+// rest (64-token block, head) value tiles, so the two run side by side instead
+// of one after the other.
+template <int MAXC>
+__global__ __launch_bounds__(256) void qk_v_append_kernel(const QkRopeParams qp,
+                                                          const VtParams vp, int qk_groups,
+                                                          int v_blocks) {
+  extern __shared__ float4 lds_qkv[];
+  const int b = blockIdx.x;
+  if (b < qk_groups) {
+    qk_norm_rope_group<MAXC>(qp, b, lds_qkv);
+  } else {
+    const int v = b - qk_groups;
+    v_append16_block(vp, v % v_blocks, v / v_blocks, reinterpret_cast<bf16_t (*)[128]>(lds_qkv));
+  }
+}
+
+static VtParams vt_params(const bf16_t* src, int ld_src, int col_off, int N, int D, int H,
+                          int hd, bf16_t* dst, bool paged, int T, const int32_t* page_table,
+                          int max_frames, int n_pages, const RowStreams& rs) {
   VtParams p;
   p.src = src;
   p.ld_src = ld_src;
@@ -553,15 +593,63 @@ hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int
   p.n_pages = n_pages;
   p.page_table = page_table;
   p.rs = rs;
-  bool groups8 = paged && T % 8 == 0 && hd <= 128 && N % 8 == 0;
-  for (int i = 0; i < rs.n && groups8; ++i)
-    groups8 = rs.s[i].len % 8 == 0 && rs.s[i].cache_len % 8 == 0 && rs.s[i].row_begin % 8 == 0;
-  if (groups8)
+  return p;
+}
+
+// the 16-byte value append applies: paged, and every 8-token group in one
+// stream and one page
+static bool vt_groups8(const VtParams& p) {
+  bool ok = p.paged && p.T % 8 == 0 && p.hd <= 128 && p.N % 8 == 0;
+  for (int i = 0; i < p.rs.n && ok; ++i)
+    ok = p.rs.s[i].len % 8 == 0 && p.rs.s[i].cache_len % 8 == 0 && p.rs.s[i].row_begin % 8 == 0;
+  return ok;
+}
+
+hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int col_off, int N,
+                              int D, int H, int hd, bf16_t* dst, bool paged, int T,
+                              const int32_t* page_table, int max_frames, int n_pages,
+                              const RowStreams& rs) {
+  if (N == 0) return hipSuccess;
+  const VtParams p = vt_params(src, ld_src, col_off, N, D, H, hd, dst, paged, T, page_table,
+                               max_frames, n_pages, rs);
+  if (vt_groups8(p))
     hipLaunchKernelGGL(v_append16_kernel, dim3((N + kVaRows - 1) / kVaRows, H), dim3(256), 0, st,
                        p);
   else
     hipLaunchKernelGGL(v_transpose_kernel, dim3((N + kVtRows - 1) / kVtRows, H), dim3(256), 0,
                        st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append(hipStream_t st, const bf16_t* qkv, int N, const RopeGeom& g,
+                            const bf16_t* g_q, const bf16_t* g_k, bf16_t* q_out,
+                            bf16_t* k_pages, bf16_t* v_pages, const int32_t* page_table,
+                            const RowStreams& rs) {
+  if (N == 0) return hipSuccess;
+  const VtParams vp = vt_params(qkv, 3 * g.D, 2 * g.D, N, g.D, g.H, g.hd, v_pages, true, g.T,
+                                page_table, g.max_frames, g.n_pages, rs);
+  const int mc = row_chunks(g.D);
+  if (!vt_groups8(vp) || mc > 4) {   // two launches
+    hipError_t e = launch_qk_norm_rope(st, qkv, N, g, g_q, g_k, q_out, k_pages, page_table, rs);
+    if (e != hipSuccess) return e;
+    return launch_v_transpose(st, qkv, 3 * g.D, 2 * g.D, N, g.D, g.H, g.hd, v_pages, true, g.T,
+                              page_table, g.max_frames, g.n_pages, rs);
+  }
+  const QkRopeParams qp = qk_params(qkv, N, g, g_q, g_k, q_out, k_pages, page_table, rs);
+  const int qk_groups = (N + kRowsPerGroup - 1) / kRowsPerGroup;
+  const int v_blocks = (N + kVaRows - 1) / kVaRows;
+  const dim3 grid(qk_groups + v_blocks * g.H);
+  const size_t lds = std::max(qk_lds_bytes(g.D), sizeof(bf16_t) * kVaRows * 128);
+  switch (mc) {
+#define ARDIT_QKV_CASE(C)                                                                     \
+    case C:                                                                                 \
+      hipLaunchKernelGGL(qk_v_append_kernel<C>, grid, dim3(256), lds, st, qp, vp, qk_groups, \
+                         v_blocks);                                                         \
+      break;
+    ARDIT_QKV_CASE(1) ARDIT_QKV_CASE(2) ARDIT_QKV_CASE(3)
+    default: ARDIT_QKV_CASE(4)
+#undef ARDIT_QKV_CASE
+  }
   return hipGetLastError();
 }
 

@@ -185,6 +185,15 @@ hipError_t launch_v_transpose(hipStream_t st, const bf16_t* src, int ld_src, int
                               const int32_t* page_table, int max_frames, int n_pages,
                               const RowStreams& rs);
 
+// QK-norm + RoPE + key append and the value append of the QKV rows (q, k, v
+// at columns 0, D, 2D of rows 3D wide) into paged storage: one launch when the
+// 16-byte value append applies and rows are at most 2048 wide, else
+// launch_qk_norm_rope then launch_v_transpose.
+hipError_t launch_kv_append(hipStream_t st, const bf16_t* qkv, int N, const RopeGeom& g,
+                            const bf16_t* g_q, const bf16_t* g_k, bf16_t* q_out,
+                            bf16_t* k_pages, bf16_t* v_pages, const int32_t* page_table,
+                            const RowStreams& rs);
+
 // rms(src row) * gain written as [H][len][hd] per stream (block at row_begin * D).
 hipError_t launch_ctx_k_layout(hipStream_t st, const bf16_t* src, int N, int D, int H, int hd,
                                const bf16_t* gain, float eps, bf16_t* dst,
