@@ -80,11 +80,15 @@ def test_ctx_kv(A):
 
 
 # --------------------------------------------------------------- kv append
-def test_kv_append_placement(A):
+# rows of 2304 (> 2048) take the two-launch append path, the tiny block the fused one
+WIDE = BlockShape(dim=2304, n_heads=18, head_dim=128, ffn_dim=256, frames=2, lat_h=4, lat_w=8)
+
+
+@pytest.mark.parametrize("sh", [TINY, WIDE], ids=["tiny", "wide"])
+def test_kv_append_placement(A, sh):
     """q~ and k~ match the oracle; values land bit-exactly in the oracle's slot
     map through a shuffled page table; nothing else of the pool changes."""
     import torch
-    sh = TINY
     rng = make_rng(43)
     caches = [2 * sh.chunk_tokens, 0, sh.chunk_tokens]
     pos0 = [6, 0, 4]
