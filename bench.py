@@ -31,7 +31,11 @@ dense fp8 peak; its quantisation pre-pass is in `value` only.
 ardit_chunk_generate of the same chunk (4 denoising steps at
 1000/750/500/250 with the sampler update between them, then the commit pass
 at t = 0), the cache being chunks 0..5 of a window of W = 7 chunks (no sink)
-while chunk 6 is generated; value = ms per chunk."""
+while chunk 6 is generated; value = ms per chunk.
+
+--append-probe only times ardit_kv_append (the elementwise key and value
+append) on 8 x 4680 rows, warm and with the caches flushed before each call,
+and prints one line with both rates."""
 from __future__ import annotations
 
 import argparse
@@ -72,6 +76,9 @@ def parse():
                    help="time whole-chunk generation (4 steps + commit) of the 1.3B-class stack")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB on the device 5 times with one kernel (counter calibration)")
+    p.add_argument("--append-probe", action="store_true",
+                   help="only time ardit_kv_append on 8 x 4680 rows of the 1.3B-class block, "
+                        "back to back and with the caches flushed before every call")
     return p.parse_args()
 
 
@@ -116,6 +123,59 @@ def copy_probe(mib):
         torch.mul(src, 1.0, out=dst)   # one elementwise kernel: reads and writes mib MiB
     torch.cuda.synchronize()
     log(f"copied {mib} MiB 5 times ({mib * (1 << 20)} bytes read and written per copy)")
+
+
+def append_probe():
+    """ardit_kv_append (QK-norm + RoPE + key append and value append, 12ND bytes)
+    over 8 streams of 4680 rows: warm (back to back) and cold (a 512 MiB buffer
+    written before each call, so neither L2 nor the 256 MB last-level cache
+    holds the operands)."""
+    import torch
+    from paper_2606_15319_amd import ardit as A
+    from workloads import WORKLOADS
+    sh = WORKLOADS["block13b"].shape
+    B, L, D, H, d, T = 8, sh.chunk_tokens, sh.dim, sh.n_heads, sh.head_dim, sh.tokens_per_frame
+    N = B * L
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(15319)
+    qkv = torch.randn((N, 3 * D), generator=g, device=dev).to(torch.bfloat16)
+    g_q = (1 + 0.02 * torch.randn((D,), generator=g, device=dev)).to(torch.bfloat16)
+    g_k = (1 + 0.02 * torch.randn((D,), generator=g, device=dev)).to(torch.bfloat16)
+    n_pages = B * sh.frames
+    kp = torch.empty((n_pages, H, T, d), dtype=torch.bfloat16, device=dev)
+    vp = torch.empty((n_pages, H, d, T), dtype=torch.bfloat16, device=dev)
+    table = torch.arange(n_pages, dtype=torch.int32, device=dev).reshape(B, sh.frames)
+    kv = A.kv_paged(kp, vp, table, n_pages, sh.frames)
+    dims = A.dims_from_shape(sh)
+    batch = A.Batch([L] * B, [0] * B, [0] * B)
+    q_out = torch.empty((N, D), dtype=torch.bfloat16, device=dev)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    call = lambda: A.ardit_kv_append(None, dims, batch, qkv, g_q, g_k, kv, q_out)  # noqa: E731
+    nbytes = 12 * N * D
+    call()
+    torch.cuda.synchronize()
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    warm_ms = e0.elapsed_time(e1) / reps
+    cold = []
+    for _ in range(reps):
+        flush.fill_(1)
+        e0.record()
+        call()
+        e1.record()
+        torch.cuda.synchronize()
+        cold.append(e0.elapsed_time(e1))
+    cold_ms = sorted(cold)[reps // 2]
+    print(json.dumps({"probe": "ardit_kv_append", "rows": N, "bytes": nbytes,
+                      "warm_ms": round(warm_ms, 4), "warm_TBps": round(nbytes / warm_ms / 1e9, 3),
+                      "cold_ms_median": round(cold_ms, 4),
+                      "cold_TBps": round(nbytes / cold_ms / 1e9, 3)}), flush=True)
 
 
 class Model:
@@ -301,6 +361,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.append_probe:
+        append_probe()
         return
     if args.chunk and (args.workload != "block13b" or args.sparsity or args.quant != "bf16"):
         print("--chunk runs the dense bf16 block13b workload only", file=sys.stderr)
