@@ -37,7 +37,7 @@ Readings where the paper is silent:
 from __future__ import annotations
 
 import math
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 
 URGENT, NORMAL, RELAXED = 0, 1, 2
 QUALITY_MODE, SPEED_RECOVERY = 0, 1

@@ -9,7 +9,6 @@ C.3), credit-aware eviction (Section 4.1) and admission (Section 3.3)."""
 import math
 
 import numpy as np
-import pytest
 
 from oracle import control_ref as K
 

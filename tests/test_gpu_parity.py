@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import oracle as O
-from harness import (BlockRun, PagedCache, NAN_BITS, dev_bf16, dev_f32, host_bits, host_f32,
+from harness import (BlockRun, PagedCache, NAN_BITS, dev_bf16, host_bits, host_f32,
                      parity, ring_page_ids, sample_rows, upload_block_weights)
 from workloads import BlockShape, WORKLOADS, bf16_round, make_rng, normal_bf16
 from workloads.gen import draw_block_case, draw_time_weights, draw_block_weights
