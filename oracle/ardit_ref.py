@@ -5,11 +5,11 @@ one chunk at a time; each chunk's generation uses the KV cache of the earlier
 chunks, and a chunk is appended to a rolling KV cache once generated; the
 cache keeps a sink plus the most recent W chunks.  Denoising runs S steps per
 chunk (Section 2.1, fidelity knobs).  The paper says nothing about the
-block's internals; this module computes the block as this build defines it
+block's internals; this module computes the block as a fixed model contract
 (adaLN-modulated RMSNorm, QKV projection, QK-RMSNorm over the full hidden
 width, 3D RoPE, self-attention of the chunk over [cache | chunk], text
-cross-attention, GELU-tanh FFN), with the readings of every silent point
-listed in the design notes.
+cross-attention, GELU-tanh FFN), each silent point taken as stated at the
+function that computes it.
 
 Conventions: every linear is y = x W^T + b with W stored [out][in];
 rms(z) = z / sqrt(mean(z^2) + eps) over the last axis; float64 throughout.

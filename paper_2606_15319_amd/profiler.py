@@ -169,7 +169,7 @@ def markdown(res, command):
     rows = res["configs"]
     fr = set(res["frontier"])
     lines = ["# Fidelity configurations: latency per chunk on one MI355X", "",
-             "Command (from the repository root on the GPU box):", "", "```", command, "```", "",
+             "Command (from the repository root, on the GPU):", "", "```", command, "```", "",
              f"One stream of the 1.3B-class stack ({res['layers']} layers, D 1536, 12 x 128 "
              "heads, FFN 8960, chunk 4680 tokens, 512 text tokens) in steady state: W cached "
              "chunks (W x 4680 keys) plus the chunk; S steps at 1000 (1 - i/S), then the "

@@ -4,8 +4,8 @@ Shapes follow the paper's setting: a chunk is three latent frames at 480p
 (Evaluation, experimental setup), the KV window W counts at most 7 earlier
 chunks and denoising uses S <= 4 steps (Appendix A, fidelity-configuration
 space).  The paper fixes no model sizes; the two model shapes below (a
-1.3B-class and a large one) and the 30 x 52 latent grid per frame are
-readings of this build, recorded in the design notes.
+1.3B-class and a large one) and the 30 x 52 latent grid per frame (480 x 832
+pixels at a 16x spatial reduction) are assumptions made here.
 
 Every value is drawn in fp32 from numpy's PCG64 seeded with 15319 + the
 workload id, then rounded to bf16 with round-to-nearest-even, so the oracle
