@@ -192,6 +192,36 @@ def test_attn_ragged_small(A, hd):
         off += n
 
 
+@pytest.mark.parametrize("mode", ["dense", "sparse", "fp8"])
+def test_attn_empty_streams_change_nothing(A, mode):
+    """Streams with no queries (their caches still paged) leave every other
+    stream's output bit-identical to a call without them, dense, block-sparse
+    and FP8 alike; a batch of empty streams only is accepted and writes
+    nothing."""
+    import torch
+    from harness import dev_i32
+    sh = BlockShape(dim=512, n_heads=4, head_dim=128, ffn_dim=1024, frames=3, lat_h=8, lat_w=8)
+    q_lens, caches = [0, 300, 0, 70], [640, 128, 0, 192]
+    pc, dims, _, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 81)
+    extra = {"dense": {}, "sparse": {"sparsity": [0.6] * 4}, "fp8": {"quant": [1] * 4}}[mode]
+    _attn(A, dims, A.Batch(q_lens, caches, **extra), q, pc.kv(A), o)
+    keep = [1, 3]
+    sub = {k: [v[b] for b in keep] for k, v in extra.items()}
+    table = dev_i32(np.ascontiguousarray(pc.table_host[keep]))
+    kv = A.kv_paged(pc.k, pc.v, table, pc.n_pages, pc.max_frames)
+    o2 = torch.full_like(o, float("nan"))
+    _attn(A, dims, A.Batch([q_lens[b] for b in keep], [caches[b] for b in keep], **sub), q, kv,
+          o2)
+    _sync()
+    assert np.array_equal(host_bits(o), host_bits(o2))
+    # empty streams only: nothing to compute, nothing written
+    o3 = torch.full_like(o, float("nan"))
+    _attn(A, dims, A.Batch([0, 0], [640, 0], **{k: v[:2] for k, v in extra.items()}), q,
+          pc.kv(A), o3)
+    _sync()
+    assert np.isnan(host_f32(o3)).all()
+
+
 def test_attn_visibility_nan_poison(A):
     """q = 0 gives the mean of exactly the visible values; every page slot
     outside [0, kv_len) holds NaN, so reading one would poison the output."""
