@@ -192,6 +192,26 @@ def test_attn_ragged_small(A, hd):
         off += n
 
 
+def test_attn_max_streams(A):
+    """The largest batch the ABI takes, 64 streams of ragged queries and caches
+    (some empty), against the oracle stream by stream."""
+    sh = BlockShape(dim=256, n_heads=2, head_dim=128, ffn_dim=512, frames=1, lat_h=4, lat_w=8)
+    assert A.ARDIT_MAX_STREAMS == 64
+    rng = np.random.default_rng(82)
+    q_lens = [int(v) for v in rng.integers(0, 90, 64)]
+    caches = [32 * int(v) for v in rng.integers(0, 5, 64)]
+    pc, dims, batch, q, o, qs, ks, vs = _attn_case(A, sh, q_lens, caches, 82)
+    _attn(A, dims, batch, q, pc.kv(A), o)
+    _sync()
+    og = host_f32(o)
+    off = 0
+    for b, n in enumerate(q_lens):
+        if n:
+            ref = O.attention(qs[b], ks[b], vs[b]).reshape(n, -1)
+            parity(og[off:off + n], ref, f"stream {b}", quantum=ref)
+        off += n
+
+
 @pytest.mark.parametrize("mode", ["dense", "sparse", "fp8"])
 def test_attn_empty_streams_change_nothing(A, mode):
     """Streams with no queries (their caches still paged) leave every other
