@@ -424,6 +424,36 @@ def test_ragged_batch_equals_single_calls(A):
                f"ragged stream {i}")
 
 
+def test_block_varlen_max_streams(A):
+    """64 streams (the ABI's maximum) of the tiny block in one varlen call:
+    caches of 0-2 chunks, different timesteps, text lengths and frame
+    positions; stream-indexed work (modulation rows, RoPE positions, page
+    slots, text blocks) checked against the oracle on eight streams."""
+    wl = WORKLOADS["tiny"]
+    sh = wl.shape
+    rng = make_rng(61)
+    pick = np.random.default_rng(61)
+    case = draw_block_case(wl)
+    case.x, case.cache_k, case.cache_v, case.ctx = [], [], [], []
+    case.cache_len, case.frame_pos0, case.t = [], [], []
+    for i in range(64):
+        c = int(pick.integers(0, 3)) * sh.chunk_tokens
+        case.x.append(normal_bf16(rng, (sh.chunk_tokens, sh.dim)))
+        case.cache_k.append(normal_bf16(rng, (c, sh.n_heads, sh.head_dim)))
+        case.cache_v.append(normal_bf16(rng, (c, sh.n_heads, sh.head_dim)))
+        case.ctx.append(normal_bf16(rng, (int(pick.integers(1, 40)), sh.dim)))
+        case.cache_len.append(c)
+        case.frame_pos0.append(c // sh.tokens_per_frame + int(pick.integers(0, 9)))
+        case.t.append(float(pick.choice([1000.0, 750.0, 500.0, 250.0])))
+    run = BlockRun(wl, A, case=case, shuffle_pages_seed=7)
+    assert run.B == 64
+    run.run()
+    _sync()
+    for b in (0, 1, 17, 31, 32, 45, 62, 63):
+        _check_block(run, b, rows=sample_rows(sh.chunk_tokens, seed=b, n_random=24),
+                     tag="64 streams")
+
+
 def test_stack_equals_repeated_blocks_and_tracks_oracle(A):
     """A 30-layer stack of the tiny block equals 30 single-block calls bit for
     bit, and stays within the parity bar of a 30-layer float64 oracle run."""
