@@ -756,7 +756,7 @@ const char* ardit_status_str(int s) {
 
 const char* ardit_last_error(void) { return g_last_error; }
 
-int ardit_version(void) { return 500; }
+int ardit_version(void) { return 501; }
 
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) try {
   ARDIT_TRY(check_dims(dims));

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     for code, name in A.STATUS.items():
         assert A.ardit_status_str(code) == name
     assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
-    assert A.ardit_version() == 500
+    assert A.ardit_version() == 501
 
 
 def _dims(**kw):
