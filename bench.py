@@ -1,25 +1,33 @@
 """Benchmark: ms per chunk-denoise-step per block on one MI355X.
 
-Workload: the 1.3B-class AR-DiT block (hidden 1536, 12 heads x 128, FFN
-8960), one stream, a 4680-token chunk (3 latent frames of 30 x 52) over a
-28080-token cache (6 earlier chunks), 512 text tokens, 30 layers.  One bench
-step is one denoising step of the chunk: the time modulation for that step's
-timestep (1000/750/500/250 in turn) followed by all 30 blocks through
-ardit_stack_fwd.  value = ms per step / 30.  Inputs are synthetic (seeded
-normal draws on the device), resident in HBM before timing starts.
+Default workload: the large AR-DiT block (hidden 5120, 40 heads x 128, FFN
+13824), one stream at chunk index 11 (frames 33..35, 3 latent frames of
+30 x 52 = 4680 tokens) over a rolling window of the 7 previous chunks (32760
+cached tokens) held in a ring of 8 chunk slots that has wrapped (physical
+pages not in logical order), 512 text tokens, 40 layers, t = 1000.  One bench
+step is one denoising step of the chunk: the time modulation for t followed
+by all 40 blocks through ardit_stack_fwd; value = ms per step / 40.  Inputs
+are synthetic (seeded normal draws on the device), resident in HBM before
+timing starts.
+
+--workload block13b runs the 1.3B-class block instead (hidden 1536, 12 x 128,
+FFN 8960, 4680 tokens over a 28080-token cache, 30 layers, t cycling
+1000/750/500/250); --workload ragged the 8-stream batch of that block (caches
+of 0..7 chunks, per-stream t, 4 layers by default).
 
 The JSON line also carries the roofline of the dominant kernel (paged
 self-attention: 4 L_q L_k D flops per launch, timed with HIP events around
 each launch on the stream it runs on) and the float64 CPU oracle timed on
-one block step of layer 0 (cpu_baseline).  roofline.traffic is the HBM bytes
-per attention launch measured with rocprofv3 counters (FETCH_SIZE and
-WRITE_SIZE, FETCH_SIZE scaled by what it reads for a plain copy of known
-size, see --copy-probe), taken from the profile summary under profiles/ when
+one block step of layer 0 (cpu_baseline; on the large block a bounded sample
+of it, see cpu_baseline).  roofline.traffic is the HBM bytes per attention
+launch measured with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE,
+FETCH_SIZE scaled by what it reads for a plain copy of known size, see
+--copy-probe), taken from the workload's profile summary under profiles/ when
 that summary was made from the current attention sources, else null.
 
 --sparsity RHO runs the same workload with block-sparse self-attention at
 sparsity RHO (the fidelity knob; every 256-query tile keeps
-ceil((1 - RHO) 512) of the 512 key tiles of 64): the step then also runs the
+ceil((1 - RHO) n) of its n key tiles of 64): the step then also runs the
 block selection, and the roofline counts the attention kernel's kept keys,
 4 L_q (n_keep 64) D flops per launch.
 
@@ -27,8 +35,8 @@ block selection, and the roofline counts the attention kernel's kept keys,
 knob): the timed kernel is the FP8 attention, priced against the 5.0 PFLOP/s
 dense fp8 peak; its quantisation pre-pass is in `value` only.
 
---chunk times whole-chunk generation instead: one bench step is one
-ardit_chunk_generate of the same chunk (4 denoising steps at
+--chunk times whole-chunk generation instead (1.3B-class stack): one bench
+step is one ardit_chunk_generate of the same chunk (4 denoising steps at
 1000/750/500/250 with the sampler update between them, then the commit pass
 at t = 0), the cache being chunks 0..5 of a window of W = 7 chunks (no sink)
 while chunk 6 is generated; value = ms per chunk.
@@ -50,8 +58,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP8_TFLOPS = 5000.0       # MI355X dense fp8 MFMA
-LAYERS = 30
 TIMESTEPS = (1000.0, 750.0, 500.0, 250.0)
+DEFAULT_LAYERS = {"large": 40, "block13b": 30, "ragged": 4}
 
 
 def log(msg):
@@ -63,15 +71,17 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--layers", type=int, default=LAYERS)
+    p.add_argument("--layers", type=int, default=None,
+                   help="layers of the stack (default: 40 large, 30 block13b, 4 ragged)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--sparsity", type=float, default=0.0, metavar="RHO",
                    help="attention sparsity rho of every stream (0: dense)")
     p.add_argument("--quant", choices=("bf16", "fp8"), default="bf16",
                    help="self-attention precision of every stream (the quantisation knob)")
-    p.add_argument("--workload", choices=("block13b", "ragged"), default="block13b",
-                   help="ragged: the 8-stream batch of 1.3B-class blocks (profiling of the "
-                        "elementwise kernels at 37440 rows); default 30 layers -> 4 there")
+    p.add_argument("--workload", choices=("large", "block13b", "ragged"), default="large",
+                   help="large: the 5120-wide block over a wrapped ring of 7 cached chunks "
+                        "(default); block13b: the 1.3B-class block; ragged: the 8-stream "
+                        "batch of 1.3B-class blocks (elementwise kernels at 37440 rows)")
     p.add_argument("--chunk", action="store_true",
                    help="time whole-chunk generation (4 steps + commit) of the 1.3B-class stack")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -82,7 +92,10 @@ def parse():
     return p.parse_args()
 
 
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_paged_block13b_hbm_traffic.md")
+def traffic_summary(workload):
+    return os.path.join(ROOT, "profiles", f"attn_paged_{workload}_hbm_traffic.md")
+
+
 ATTN_SOURCES = ("paper_2606_15319_amd/csrc/k_attn.hip", "paper_2606_15319_amd/csrc/launch.h",
                 "paper_2606_15319_amd/csrc/common.h")
 
@@ -96,12 +109,12 @@ def attn_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per attention launch from the counter summary, or None when the
-    summary is missing or was made from other attention sources."""
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the workload's counter summary, or
+    None when the summary is missing or was made from other attention sources."""
     try:
         fields = {}
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(traffic_summary(workload)) as f:
             for line in f:
                 if ":" in line and line.startswith("- "):
                     k, v = line[2:].split(":", 1)
@@ -180,67 +193,73 @@ def append_probe():
 
 class Model:
     """Weights, pages and text K/V of every layer for a batch of streams (one
-    chunk each, stream b over cache_lens[b] cached tokens), drawn on the device."""
+    chunk each, stream b over cache_lens[b] cached tokens in pages page_ids[b],
+    logical order), drawn on the device."""
 
-    def __init__(self, A, sh, n_layers, cache_lens, ctx_len, dev, rho=0.0, timesteps=None,
-                 fp8=False):
+    def __init__(self, A, wl, n_layers, dev, rho=0.0, timesteps=None, fp8=False):
         import torch
+        from workloads import stream_page_ids
+        sh = wl.shape
         self.A, self.sh, self.n_layers = A, sh, n_layers
-        D, F, H, d = sh.dim, sh.ffn_dim, sh.n_heads, sh.head_dim
+        D, H, d = sh.dim, sh.n_heads, sh.head_dim
         T = sh.tokens_per_frame
+        cache_lens = [c * sh.chunk_tokens for c in wl.cache_chunks]
         B = len(cache_lens)
         self.B = B
-        self.cache_lens, self.ctx_len = list(cache_lens), ctx_len
+        self.cache_lens, self.ctx_len = list(cache_lens), wl.ctx_len
         self.cache_len = cache_lens[0]
-        frames = [c // T + sh.frames for c in cache_lens]
-        self.frames = sum(frames)
+        self.frame_pos0 = list(wl.frame_pos0)
+        page_ids, n_pages = stream_page_ids(wl)
+        self.page_ids, self.n_pages = page_ids, n_pages
+        max_frames = max(len(p) for p in page_ids)
         self.dims = A.dims_from_shape(sh)
         self.rho = rho
         self.timesteps = timesteps
         self.fp8 = fp8
-        self.batch = A.Batch([sh.chunk_tokens] * B, cache_lens, [c // T for c in cache_lens],
-                             [ctx_len] * B, sparsity=[rho] * B, quant=[1 if fp8 else 0] * B)
+        self.batch = A.Batch([sh.chunk_tokens] * B, cache_lens, self.frame_pos0,
+                             [wl.ctx_len] * B, sparsity=[rho] * B, quant=[1 if fp8 else 0] * B)
         self.ws_bytes = A.ardit_workspace_size(self.dims, self.batch)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
         from workloads.gen import block_weight_shapes, GAIN_NAMES
         shapes = block_weight_shapes(sh)
         self.w, self.kv, self.ctx_k, self.ctx_v, self.keep = [], [], [], [], []
-        table = torch.zeros((B, max(frames)), dtype=torch.int32)
-        first = 0
-        for b, nf in enumerate(frames):
-            table[b, :nf] = torch.arange(first, first + nf, dtype=torch.int32)
-            first += nf
+        table = torch.zeros((B, max_frames), dtype=torch.int32)
+        for b, ids in enumerate(page_ids):
+            table[b, :len(ids)] = torch.tensor(ids, dtype=torch.int32)
         self.table = table.to(dev)
+        ctx_len = wl.ctx_len
         for layer in range(n_layers):
             g = torch.Generator(device=dev)
-            g.manual_seed(15319 + 3 + 1000 * layer)
+            g.manual_seed(15319 + wl.wid + 1000 * layer)
             wd = {}
             for name, shp in shapes.items():
                 t = torch.randn(shp, generator=g, device=dev, dtype=torch.float32) * 0.02
                 if name in GAIN_NAMES:
                     t += 1.0
                 wd[name] = t if name == "mod_table" else t.to(torch.bfloat16)
-            kp = torch.randn((self.frames, H, T, d), generator=g, device=dev).to(torch.bfloat16)
-            vp = torch.randn((self.frames, H, d, T), generator=g, device=dev).to(torch.bfloat16)
+                del t
+            kp = torch.randn((n_pages, H, T, d), generator=g, device=dev).to(torch.bfloat16)
+            vp = torch.randn((n_pages, H, d, T), generator=g, device=dev).to(torch.bfloat16)
             ctx = torch.randn((B * ctx_len, D), generator=g, device=dev).to(torch.bfloat16)
             ck = torch.empty(B * ctx_len * D, dtype=torch.bfloat16, device=dev)
             cv = torch.empty_like(ck)
             w = A.block_weights(wd)
             A.ardit_ctx_kv(None, self.dims, self.batch, ctx, w, ck, cv, self.ws, self.ws_bytes)
             self.w.append(w)
-            self.kv.append(A.kv_paged(kp, vp, self.table, self.frames, max(frames)))
+            self.kv.append(A.kv_paged(kp, vp, self.table, n_pages, max_frames))
             self.ctx_k.append(ck)
             self.ctx_v.append(cv)
             self.keep.append((wd, kp, vp, ctx))
         g = torch.Generator(device=dev)
-        g.manual_seed(15319 + 3)
+        g.manual_seed(15319 + wl.wid)
         tshapes = {"w_t1": (D, 256), "b_t1": (D,), "w_t2": (D, D), "b_t2": (D,),
                    "w_m": (6 * D, D), "b_m": (6 * D,)}
         self.tw_dev = {k: (torch.randn(s, generator=g, device=dev) * 0.02).to(torch.bfloat16)
                        for k, s in tshapes.items()}
         self.tw = A.time_weights(self.tw_dev)
+        self.step_ts = TIMESTEPS if wl.name == "block13b" else (float(wl.timesteps[0]),)
         self.xs = [torch.randn((B * sh.chunk_tokens, D), generator=g, device=dev).to(torch.bfloat16)
-                   for _ in TIMESTEPS]
+                   for _ in self.step_ts]
         self.mod = torch.empty((B, 6, D), dtype=torch.float32, device=dev)
         self.out = torch.empty_like(self.xs[0])
 
@@ -268,16 +287,21 @@ class Model:
 
     def step(self, k):
         A = self.A
-        ts = self.timesteps or [TIMESTEPS[k % len(TIMESTEPS)]] * self.B
+        ts = self.timesteps or [self.step_ts[k % len(self.step_ts)]] * self.B
         A.ardit_time_mod(None, self.dims, ts, self.tw, self.mod, self.ws, self.ws_bytes)
         A.ardit_stack_fwd(None, self.dims, self.batch, self.xs[k % len(self.xs)], self.kv,
                           self.mod, self.ctx_k, self.ctx_v, self.w, self.out, self.ws,
                           self.ws_bytes)
 
 
-def cpu_baseline(model):
-    """The float64 oracle on one block step (layer 0, step 0) of the same
-    workload, on the host cores, with the layer's own inputs copied back."""
+def cpu_baseline(model, sample_every=1):
+    """The float64 oracle on one block step (layer 0, the first timestep) of
+    the same workload, on the host cores, with the layer's own inputs copied
+    back.  sample_every > 1 bounds the CPU time: the oracle always computes the
+    keys and values of the whole chunk, then the rest of the block only for the
+    rows it is asked for, so it is timed twice -- on query row 0 alone (t1) and
+    on every sample_every-th row (n rows, tn) -- and the full step is
+    extrapolated linearly in the rows, t1 + (tn - t1) (L_q - 1) / (n - 1)."""
     import numpy as np
     import torch
 
@@ -293,31 +317,48 @@ def cpu_baseline(model):
     wd, kp, vp, ctx = model.keep[0]
     w = {k: host(v) for k, v in wd.items()}
     tw = {k: host(v) for k, v in model.tw_dev.items()}
-    H, d, T = sh.n_heads, sh.head_dim, sh.tokens_per_frame
+    H, d, T, Lq = sh.n_heads, sh.head_dim, sh.tokens_per_frame, sh.chunk_tokens
     nf = model.cache_len // T
-    ck = np.transpose(host(kp[:nf]), (0, 2, 1, 3)).reshape(-1, H, d)
-    cv = np.transpose(host(vp[:nf]), (0, 3, 1, 2)).reshape(-1, H, d)
-    x = host(model.xs[0])
-    ctxh = host(ctx)
+    pages = torch.tensor(model.page_ids[0][:nf], dtype=torch.long, device=kp.device)
+    ck = np.transpose(host(kp.index_select(0, pages)), (0, 2, 1, 3)).reshape(-1, H, d)
+    cv = np.transpose(host(vp.index_select(0, pages)), (0, 3, 1, 2)).reshape(-1, H, d)
+    x = host(model.xs[0])[:Lq]
+    ctxh = host(ctx)[:model.ctx_len]
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
     t0 = time.perf_counter()
-    m_t = O.time_modulation(TIMESTEPS[0], tw, sh.dim)
+    m_t = O.time_modulation(model.step_ts[0], tw, sh.dim)
     kc, vc = O.context_kv(ctxh, w, sh.eps)
     t_ctx = time.perf_counter()
-    O.block_forward(x, ck, cv, model.cache_len // T, m_t, kc, vc, w, sh, rho=model.rho,
-                    fp8=model.fp8)
-    t1 = time.perf_counter()
-    return {"value": round((t1 - t_ctx) * 1e3, 1), "unit": "ms per chunk-denoise-step per block",
-            "cores": int(threads), "kind": "oracle",
-            "sample": ("one full block step (layer 0, t=1000) of the same workload: 4680 queries "
-                       f"over 32760 keys{' at sparsity %g' % model.rho if model.rho else ''}"
-                       f"{' with FP8 attention' if model.fp8 else ''}, "
-                       "float64 numpy; text K/V and time modulation "
-                       f"({(t_ctx - t0) * 1e3:.0f} ms) excluded as on the GPU path")}
+
+    def run(rows):
+        a = time.perf_counter()
+        O.block_forward(x, ck, cv, model.frame_pos0[0], m_t, kc, vc, w, sh, rows=rows,
+                        rho=model.rho, fp8=model.fp8)
+        return time.perf_counter() - a
+
+    what = (f"one block step (layer 0, t={model.step_ts[0]:g}) of the same workload: "
+            f"{Lq} queries over {model.cache_len + Lq} keys"
+            f"{' at sparsity %g' % model.rho if model.rho else ''}"
+            f"{' with FP8 attention' if model.fp8 else ''}, float64 numpy; text K/V and time "
+            f"modulation ({(t_ctx - t0) * 1e3:.0f} ms) excluded as on the GPU path")
+    if sample_every <= 1:
+        ms = run(None) * 1e3
+        sample = "measured: " + what
+    else:
+        rows = np.arange(0, Lq, sample_every)
+        t1 = run(np.array([0]))
+        tn = run(rows)
+        ms = (t1 + (tn - t1) * (Lq - 1) / (len(rows) - 1)) * 1e3
+        sample = (f"extrapolated from a sample of {what}: the oracle timed on query row 0 "
+                  f"({t1 * 1e3:.0f} ms) and on every {sample_every}th row ({len(rows)} rows, "
+                  f"{tn * 1e3:.0f} ms; keys and values of the whole chunk in both), linear in "
+                  f"the rows to all {Lq}")
+    return {"value": round(ms, 1), "unit": "ms per chunk-denoise-step per block",
+            "cores": int(threads), "kind": "oracle", "sample": sample}
 
 
 def kernel_breakdown(A, model, args, sh, cache_lens):
@@ -353,6 +394,30 @@ def kernel_breakdown(A, model, args, sh, cache_lens):
                     "outside the timed region"}
 
 
+def workload_name(wl, args):
+    sh = wl.shape
+    if args.chunk:
+        return ("whole-chunk generation, 1.3B-class AR-DiT stack: D=1536, 12x128 heads, "
+                f"FFN 8960, {args.layers} layers, chunk 6 of a stream (4680 tokens, "
+                "3x30x52) over a window of W=7 chunks holding chunks 0..5 (28080 "
+                "tokens), 512 text tokens, 4 denoising steps at t=1000/750/500/250 "
+                "with the sampler update, then the commit pass at t=0")
+    if wl.name == "ragged":
+        return ("ragged batch of 8 streams of the 1.3B-class block (D=1536, 12x128 "
+                "heads, FFN 8960), one 4680-token chunk each over caches of "
+                f"{'/'.join(str(c) for c in wl.cache_chunks)} chunks, 512 text tokens "
+                f"each, {args.layers} layers, per-stream t")
+    if wl.name == "large":
+        return (f"large AR-DiT block: D={sh.dim}, {sh.n_heads}x{sh.head_dim} heads, FFN "
+                f"{sh.ffn_dim}, chunk 11 of a stream (4680 tokens, 3x30x52, frames 33-35) over "
+                "a rolling window of the 7 previous chunks (32760 tokens) in a wrapped ring of "
+                f"8 chunk slots, 512 text tokens, {args.layers} layers, one denoising step at "
+                "t=1000")
+    return ("1.3B-class AR-DiT block: D=1536, 12x128 heads, FFN 8960, chunk 4680 "
+            "tokens (3x30x52) over a 28080-token cache, 512 text tokens, "
+            f"{args.layers} layers, t=1000/750/500/250")
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -365,9 +430,13 @@ def main():
     if args.append_probe:
         append_probe()
         return
+    if args.chunk and args.workload == "large":
+        args.workload = "block13b"
     if args.chunk and (args.workload != "block13b" or args.sparsity or args.quant != "bf16"):
         print("--chunk runs the dense bf16 block13b workload only", file=sys.stderr)
         sys.exit(2)
+    if args.layers is None:
+        args.layers = DEFAULT_LAYERS[args.workload]
     import torch
     from paper_2606_15319_amd import ardit as A
     from workloads import WORKLOADS
@@ -378,10 +447,8 @@ def main():
     sh = wl.shape
     cache_lens = [c * sh.chunk_tokens for c in wl.cache_chunks]
     ragged = args.workload == "ragged"
-    if ragged and args.layers == LAYERS:
-        args.layers = 4
-    log(f"drawing {args.layers} layers on the device")
-    model = Model(A, sh, args.layers, cache_lens, wl.ctx_len, dev, rho=args.sparsity,
+    log(f"drawing {args.layers} layers of the {args.workload} workload on the device")
+    model = Model(A, wl, args.layers, dev, rho=args.sparsity,
                   timesteps=[float(t) for t in wl.timesteps] if ragged else None,
                   fp8=args.quant == "fp8")
     if args.chunk:
@@ -413,6 +480,7 @@ def main():
     L_q, D = sh.chunk_tokens, sh.dim
     L_k = cache_lens[0] + L_q
     attn_flops = 0.0
+    keys = L_k
     for c in cache_lens:
         n_tiles = (c + L_q + 63) // 64
         keys = c + L_q
@@ -430,7 +498,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline and not ragged:
         log("timing the CPU oracle on one block step")
-        cpu = cpu_baseline(model)
+        cpu = cpu_baseline(model, sample_every=4 if args.workload == "large" else 1)
         if args.chunk:
             # one block pass, scaled to the chunk's layers x passes
             cpu["value"] = round(cpu["value"] * args.layers * passes, 1)
@@ -438,21 +506,6 @@ def main():
             cpu["sample"] += (f"; scaled by {args.layers} layers x {passes} passes to a chunk "
                               "(extrapolated)")
         log(f"oracle: {cpu['value']} ms on {cpu['cores']} threads")
-    if ragged:
-        workload_name = ("ragged batch of 8 streams of the 1.3B-class block (D=1536, 12x128 "
-                         "heads, FFN 8960), one 4680-token chunk each over caches of "
-                         f"{'/'.join(str(c) for c in wl.cache_chunks)} chunks, 512 text tokens "
-                         f"each, {args.layers} layers, per-stream t")
-    else:
-        workload_name = ("1.3B-class AR-DiT block: D=1536, 12x128 heads, FFN 8960, chunk 4680 "
-                         "tokens (3x30x52) over a 28080-token cache, 512 text tokens, "
-                         f"{args.layers} layers, t=1000/750/500/250")
-    if args.chunk:
-        workload_name = ("whole-chunk generation, 1.3B-class AR-DiT stack: D=1536, 12x128 heads, "
-                         f"FFN 8960, {args.layers} layers, chunk 6 of a stream (4680 tokens, "
-                         "3x30x52) over a window of W=7 chunks holding chunks 0..5 (28080 "
-                         "tokens), 512 text tokens, 4 denoising steps at t=1000/750/500/250 "
-                         "with the sampler update, then the commit pass at t=0")
     peak = PEAK_FP8_TFLOPS if args.quant == "fp8" else PEAK_BF16_TFLOPS
     line = {
         "metric": "ms per chunk" if args.chunk else "ms per chunk-denoise-step per block",
@@ -468,7 +521,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if args.quant == "bf16" else "bf16 (attention fp8 e4m3)",
         "data": "synthetic (seeded normal draws, random-init weights)",
-        "config": {"workload": workload_name,
+        "config": {"workload": workload_name(wl, args),
                    "layers": args.layers, "chunk_tokens": L_q,
                    "kv_tokens": L_k if not ragged else [c + L_q for c in cache_lens],
                    "ctx_tokens": wl.ctx_len, "sparsity": args.sparsity,
@@ -476,8 +529,9 @@ def main():
                    "attended_keys": keys if not ragged else None},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                     "traffic": (None if (args.sparsity or ragged or args.quant == "fp8")
-                                 else measured_traffic()),
+                     "traffic": (None if (args.sparsity or ragged or args.quant == "fp8"
+                                          or args.chunk)
+                                 else measured_traffic(args.workload)),
                      "kernel": (("FP8 " if args.quant == "fp8" else "")
                                 + ("block-sparse " if args.sparsity else "")
                                 + "paged self-attention"),

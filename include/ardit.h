@@ -7,9 +7,10 @@
  * stream's KV cache of earlier chunks plus the chunk itself, and the chunk is
  * appended to that cache once generated (paper, Section 2.1, "AR-DiT").  The
  * cache is paged at latent-frame granularity behind a logical page table, and
- * different streams hold different cache lengths (Section 3.2, State Plane,
- * and Section 4.4, unified KV management).  The block's internals are not
- * given by the paper; this library computes, per block and per stream b:
+ * different streams hold different cache lengths (Section 3.2, the State
+ * Plane paragraph and its footnote; Section 4.4, "Unified KV management").
+ * The block's internals are not given by the paper; this library computes,
+ * per block and per stream b:
  *
  *   M      = mod[b] + mod_table                       rows: shift1 scale1 gate1 shift2 scale2 gate2
  *   h1     = rms(x) * (1 + scale1) + shift1
@@ -122,7 +123,10 @@ typedef struct {
   void* k_pages;               /* [n_pages][H][T][d] bf16 */
   void* v_pages;               /* [n_pages][H][d][T] bf16 */
   const int32_t* page_table;   /* [n_streams][max_frames] int32, physical page of each logical frame */
-  int32_t n_pages;             /* pages in the pool; out-of-range table entries are clamped into it */
+  int32_t n_pages;             /* pages in the pool.  A table entry outside [0, n_pages) is a caller
+                                  error: reads clamp it into the pool, writes skip it (the chunk's
+                                  keys/values for that frame are dropped, no other page changes);
+                                  ardit_debug_checks(1) rejects such a table before any launch */
   int32_t max_frames;          /* row length of page_table */
 } ardit_kv_paged;
 
@@ -154,14 +158,16 @@ typedef struct {
 const char* ardit_status_str(int status);
 /* Detail of the calling thread's last failed call ("" if none). */
 const char* ardit_last_error(void);
-/* ABI version (major * 100 + minor). */
+/* ABI version (major * 100 + minor): 502. */
 int ardit_version(void);
 
 /* Workspace bytes needed by any call below for this geometry and batch
  * (block, stack, context and time-modulation calls share one workspace). */
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes);
 
-/* Time modulation, once per stream per denoising step: sinusoid of t (256
+/* Time modulation, once per stream per denoising step (the timestep that
+ * conditions each of the S denoising steps of a chunk, Section 2.1; the
+ * paper gives no embedding, this is the DiT-family form): sinusoid of t (256
  * features: cos then sin of t * 10000^(-k/128)), then
  * m = W_m SiLU(W_t2 SiLU(W_t1 s + b_t1) + b_t2) + b_m.
  * t_host: host [n_streams] timesteps.  mod_out: device fp32 [n_streams][6][D]. */
@@ -169,7 +175,8 @@ int ardit_time_mod(hipStream_t stream, const ardit_dims* dims, int32_t n_streams
                    const float* t_host, const ardit_time_weights* tw, float* mod_out,
                    void* ws, size_t ws_bytes);
 
-/* Text keys/values of each stream for one block: K_c = rms(ctx W_ck^T + b_ck) * g_ck,
+/* Text keys/values of each stream for one block (the conditioning embeddings
+ * the DiT attends to, Section 2.1, "Video Generation"): K_c = rms(ctx W_ck^T + b_ck) * g_ck,
  * V_c = ctx W_cv^T + b_cv, written in the layout described above.
  * ctx: device bf16 [sum ctx_lens][D], streams packed in order.  Only
  * batch->n_streams and batch->ctx_lens are read. */
@@ -177,7 +184,9 @@ int ardit_ctx_kv(hipStream_t stream, const ardit_dims* dims, const ardit_batch* 
                  const void* ctx, const ardit_block_weights* w, void* ctx_k, void* ctx_v,
                  void* ws, size_t ws_bytes);
 
-/* The QK-norm / RoPE / append step alone: from packed projections qkv
+/* The QK-norm / RoPE / append step alone (a chunk's keys and values enter the
+ * stream's rolling cache, Section 2.1, "AR-DiT"; frame pages behind the
+ * logical page table, Section 4.4): from packed projections qkv
  * (device bf16 [sum q_lens][3D], columns q | k | v), writes q~ (device bf16
  * [sum q_lens][D]) and the chunk's k~ and v into logical slots
  * [cache_len, cache_len + q_len) of each stream's pages.  g_q, g_k: device
@@ -186,7 +195,10 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
                     const void* qkv, const void* g_q, const void* g_k,
                     const ardit_kv_paged* kv, void* q_out);
 
-/* Paged attention alone: o = softmax(q K^T / sqrt(d)) V per stream and head
+/* Paged attention alone (a chunk attends to the KV cache of the stream's
+ * earlier chunks and to itself, Section 2.1, "AR-DiT"; pages per latent frame,
+ * Section 4.4; per-stream cache lengths, Section 3.2 footnote):
+ * o = softmax(q K^T / sqrt(d)) V per stream and head
  * over logical keys [0, cache_len + q_len) of the stream's pages (the chunk's
  * own keys must already be in the pages).  q, o: device bf16 [sum q_lens][H][d].
  * ws / ws_bytes as for the block calls (ardit_workspace_size of this batch):
@@ -230,7 +242,10 @@ int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_
                         const void* q, const ardit_kv_paged* kv, int32_t* blocks,
                         int32_t row_stride, void* ws, size_t ws_bytes);
 
-/* One block, one stream (dense self-attention).  x, out: device bf16 [L_q][D] (L_q = frames_per_chunk * T);
+/* One block, one stream (dense self-attention): one denoising step of one DiT
+ * block on a chunk over the stream's KV cache (Section 2.1, "AR-DiT"; the
+ * block internals are the contract at the top of this file).
+ * x, out: device bf16 [L_q][D] (L_q = frames_per_chunk * T);
  * kv.page_table has one row.  mod: device fp32 [6][D] (from ardit_time_mod).
  * ctx_k / ctx_v from ardit_ctx_kv with ctx_len text tokens.  Writes the
  * chunk's keys/values into slots [cache_len, cache_len + L_q); the caller
@@ -241,7 +256,8 @@ int ardit_block_fwd(hipStream_t stream, const ardit_dims* dims, const void* x,
                     const ardit_block_weights* w, void* out, void* ws, size_t ws_bytes);
 
 /* One block over a ragged batch of streams sharing the weights (one GPU's share
- * of the streams).  x, out: device bf16 [sum q_lens][D]; mod: device fp32
+ * of the streams; streams hold different KV lengths, Section 3.2 footnote, and
+ * a worker serves several streams, Section 3.1).  x, out: device bf16 [sum q_lens][D]; mod: device fp32
  * [n_streams][6][D]; page_table rows follow the batch order.  Streams with
  * batch->sparsity > 0 run block-sparse self-attention (ardit_sparse_select). */
 int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
@@ -249,7 +265,8 @@ int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ard
                            const void* ctx_k, const void* ctx_v, const ardit_block_weights* w,
                            void* out, void* ws, size_t ws_bytes);
 
-/* n_layers blocks applied in sequence (one denoising step of the stack).
+/* n_layers blocks applied in sequence (one denoising step of the DiT, Section
+ * 2.1: the model denoises the chunk's latent over S such steps).
  * kv, w, ctx_k, ctx_v: host arrays of n_layers entries.  x is not modified. */
 int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                     int32_t n_layers, const void* x, const ardit_kv_paged* kv, const float* mod,
@@ -332,6 +349,17 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
 int ardit_timing_enable(int enable);
 int ardit_timing_collect(int32_t* launches, double* total_ms);
 int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms);
+
+/* Debug validation of page tables (off by default; for callers that want a
+ * bad table reported rather than silently dropped or clamped).  With
+ * ardit_debug_checks(1) every call that reads a page table first copies it to
+ * the host on the call's stream and synchronises that stream, then returns
+ * ARDIT_ECAPACITY when an entry that a stream reads or writes lies outside
+ * [0, n_pages), and ARDIT_EINVAL when a page that the call writes (a chunk's
+ * frames) is written by two streams, twice by one, or read as cache by another
+ * stream; nothing is enqueued then.  The synchronisation makes it unsuitable
+ * for timed or captured runs.  0 turns it off; other values: ARDIT_EINVAL. */
+int ardit_debug_checks(int enable);
 
 #ifdef __cplusplus
 }

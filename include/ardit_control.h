@@ -1,9 +1,8 @@
 /*
  * ardit_control.h -- the playout-slack controller of libardit (host code).
  *
- * The decisions that pick which stream's chunk runs next, where, and at which
- * fidelity (paper, Sections 3-5): service credit, urgency tiers and dispatch
- * order, credit-aware eviction, re-homing, the elastic-SP donor, admission, and
+ * The decisions that pick which stream's chunk runs next and at which fidelity
+ * (paper, Sections 3-5): service credit, urgency tiers and dispatch order, and
  * Bi-Modal Pareto Routing over the profiled fidelity configurations.  Every
  * call is plain host computation on caller-owned host arrays: no HIP call, no
  * allocation that outlives the call, no state kept between calls.  Times are
@@ -61,21 +60,10 @@ int ardit_bmpr_select(int32_t n_cfgs, const ardit_fidelity* cfgs, int32_t n_fron
 
 /* Per-stream state the controller reads at a tick. */
 typedef struct {
-  int32_t worker;            /* current home worker */
-  int32_t sp_donor;          /* donor worker of the stream's SP2 group, -1 when none */
+  int32_t worker;            /* home worker (0 .. n_workers - 1) */
   double slack_ms;           /* P: playable buffer left */
   double remaining_ms;       /* R: estimated time to finish the running chunk, 0 if not running */
-  double cooldown_until_ms;  /* re-homing cooldown end (controller clock), -inf when none */
 } ardit_stream_state;
-
-typedef struct {
-  int32_t n_workers;
-  int32_t gpus_per_node;     /* workers w and w' share a node when w / g == w' / g */
-  int32_t cap_send;          /* migrations out of one worker per tick (2) */
-  int32_t cap_recv;          /* migrations into one worker per tick (1) */
-  double cooldown_ms;        /* after a migration (60000) */
-  double now_ms;             /* controller clock */
-} ardit_ctl_params;
 
 /* What a tick decides for one stream. */
 typedef struct {
@@ -83,55 +71,22 @@ typedef struct {
   int32_t mode;              /* ardit_bmpr_mode */
   int32_t tier;              /* ardit_tier under cfg */
   int32_t queue_pos;         /* 0-based position in its worker's dispatch order */
-  int32_t rehome_to;         /* destination worker planned this tick, -1 */
-  int32_t sp_donor;          /* donor after this tick, -1 */
   double credit_ms;          /* C = P - (R + L_cfg) */
-  double cooldown_until_ms;  /* updated when the stream is re-homed */
 } ardit_stream_decision;
 
-/* One control tick (Appendix C.1 order):
- *  1. per stream: cfg by BMPR with budget P - R; credit C = P - (R + L_cfg);
- *     tier URGENT when C < 2 L_cfg, RELAXED when C > 4 L_cfg, else NORMAL
- *     (Sections 3.1, 4.1);
- *  2. dispatch order per worker: ascending credit, then stream index;
- *  3. re-homing (Section 4.2 and its algorithm; Appendix C.2): senders are
- *     workers holding at least two URGENT streams, most URGENT streams first
- *     (then lower id); receivers are workers with no URGENT or NORMAL stream
- *     (idle ones included), tried same-node first, then by id; while the
- *     sender has sent fewer than cap_send and the receiver received fewer
- *     than cap_recv, the sender's lowest-credit URGENT stream that is not in
- *     cooldown, not in an SP2 group and not yet moved goes to that receiver
- *     and enters cooldown until now + cooldown_ms;
- *  4. elastic SP (Section 4.3; Appendix C.3): a stream keeps its donor until
- *     C >= 2 L_cfg (NORMAL), then releases it; each stream with C < 0 that has
- *     no donor and is not being re-homed, in ascending credit order, borrows
- *     the highest-credit worker on its own node (a worker's credit: the lowest
- *     of its streams', +inf when idle; ties to the lower id) that has no
- *     URGENT or NORMAL stream, is not its own worker, is not lending and did
- *     not receive a migration this tick; none is borrowed when there is none.
+/* One control tick over the streams of n_workers workers (Appendix C.1 order,
+ * its first two decisions):
+ *  1. per stream: cfg by BMPR with budget P - R; credit C = P - (R + L_cfg)
+ *     (Section 3.1); tier URGENT when C < 2 L_cfg, RELAXED when C > 4 L_cfg,
+ *     else NORMAL (Section 4.1);
+ *  2. dispatch order per worker: ascending credit, then stream index
+ *     (Section 4.1, credit-ordered queues).
  * streams / out: n_streams entries.  EINVAL on a malformed argument (worker
- * or donor out of range, non-finite slack or remaining time, empty
- * frontier). */
-int ardit_control_tick(const ardit_ctl_params* params, int32_t n_cfgs,
-                       const ardit_fidelity* cfgs, int32_t n_frontier, const int32_t* frontier,
-                       double q_floor, int32_t n_streams, const ardit_stream_state* streams,
+ * out of range, non-finite slack or remaining time, empty frontier). */
+int ardit_control_tick(int32_t n_workers, int32_t n_cfgs, const ardit_fidelity* cfgs,
+                       int32_t n_frontier, const int32_t* frontier, double q_floor,
+                       int32_t n_streams, const ardit_stream_state* streams,
                        ardit_stream_decision* out);
-
-/* Credit-aware eviction (Section 4.1): to make room for need_pages of stream
- * `requester` when free_pages are free, evict resident streams other than the
- * requester (resident_pages[i] > 0) in order of credit descending (ties: the
- * higher index first) until the pages fit.  Writes the evicted indices in
- * order to evict[] (room for n) and their count.  ECAPACITY (nothing written)
- * when evicting every other resident stream would still leave too few. */
-int ardit_evict_for(int32_t n, const double* credits, const int32_t* resident_pages,
-                    int32_t requester, int64_t free_pages, int64_t need_pages, int32_t* evict,
-                    int32_t* n_evict);
-
-/* Admission (Section 3.3): the home worker is the one with the fewest
- * streams (lowest id on ties); the initial slack (the time-to-first-chunk
- * budget) is 4x the estimated first-chunk time. */
-int ardit_admit(int32_t n_workers, const int32_t* streams_per_worker, double first_chunk_ms,
-                int32_t* home, double* slack_ms);
 
 #ifdef __cplusplus
 }

@@ -82,19 +82,12 @@ class ardit_fidelity(C.Structure):
 
 
 class ardit_stream_state(C.Structure):
-    _fields_ = [("worker", C.c_int32), ("sp_donor", C.c_int32), ("slack_ms", C.c_double),
-                ("remaining_ms", C.c_double), ("cooldown_until_ms", C.c_double)]
-
-
-class ardit_ctl_params(C.Structure):
-    _fields_ = [("n_workers", C.c_int32), ("gpus_per_node", C.c_int32), ("cap_send", C.c_int32),
-                ("cap_recv", C.c_int32), ("cooldown_ms", C.c_double), ("now_ms", C.c_double)]
+    _fields_ = [("worker", C.c_int32), ("slack_ms", C.c_double), ("remaining_ms", C.c_double)]
 
 
 class ardit_stream_decision(C.Structure):
     _fields_ = [("cfg", C.c_int32), ("mode", C.c_int32), ("tier", C.c_int32),
-                ("queue_pos", C.c_int32), ("rehome_to", C.c_int32), ("sp_donor", C.c_int32),
-                ("credit_ms", C.c_double), ("cooldown_until_ms", C.c_double)]
+                ("queue_pos", C.c_int32), ("credit_ms", C.c_double)]
 
 
 _vp, _i32, _sz = C.c_void_p, C.c_int32, C.c_size_t
@@ -132,15 +125,13 @@ _SIGS = {
                                         _P(C.c_double)]),
     "ardit_bmpr_select": (C.c_int, [_i32, _P(ardit_fidelity), _i32, _P(_i32), C.c_double,
                                     C.c_double, _P(_i32), _P(_i32)]),
-    "ardit_control_tick": (C.c_int, [_P(ardit_ctl_params), _i32, _P(ardit_fidelity), _i32,
-                                     _P(_i32), C.c_double, _i32, _P(ardit_stream_state),
+    "ardit_control_tick": (C.c_int, [_i32, _i32, _P(ardit_fidelity), _i32, _P(_i32),
+                                     C.c_double, _i32, _P(ardit_stream_state),
                                      _P(ardit_stream_decision)]),
-    "ardit_evict_for": (C.c_int, [_i32, _P(C.c_double), _P(_i32), _i32, C.c_int64, C.c_int64,
-                                  _P(_i32), _P(_i32)]),
-    "ardit_admit": (C.c_int, [_i32, _P(_i32), C.c_double, _P(_i32), _P(C.c_double)]),
     "ardit_timing_enable": (C.c_int, [C.c_int]),
     "ardit_timing_collect": (C.c_int, [_P(_i32), _P(C.c_double)]),
     "ardit_timing_collect_kind": (C.c_int, [_i32, _P(_i32), _P(C.c_double)]),
+    "ardit_debug_checks": (C.c_int, [C.c_int]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -373,6 +364,10 @@ def ardit_timing_collect_kind(kind):
     return n.value, ms.value
 
 
+def ardit_debug_checks(enable):
+    _check(_lib.ardit_debug_checks(int(enable)), "ardit_debug_checks")
+
+
 def ardit_timing_collect():
     n = C.c_int32(0)
     ms = C.c_double(0.0)
@@ -414,41 +409,16 @@ def ardit_bmpr_select(cfgs, frontier, q_floor, budget_ms):
     return c.value, m.value
 
 
-def ardit_control_tick(params: dict, cfgs, frontier, q_floor, streams):
-    """params: n_workers, gpus_per_node, cap_send, cap_recv, cooldown_ms, now_ms;
-    streams: sequence of (worker, sp_donor, slack_ms, remaining_ms, cooldown_until_ms).
-    Returns a list of ardit_stream_decision."""
-    p = ardit_ctl_params(int(params["n_workers"]), int(params.get("gpus_per_node", 8)),
-                         int(params.get("cap_send", 2)), int(params.get("cap_recv", 1)),
-                         float(params.get("cooldown_ms", 60000.0)), float(params.get("now_ms", 0.0)))
+def ardit_control_tick(n_workers, cfgs, frontier, q_floor, streams):
+    """streams: sequence of (worker, slack_ms, remaining_ms).  Returns a list of
+    ardit_stream_decision."""
     arr = cfgs if isinstance(cfgs, C.Array) else fidelity_array(cfgs)
     f = (C.c_int32 * len(frontier))(*frontier)
     n = len(streams)
     st = (ardit_stream_state * max(n, 1))()
     for i, s in enumerate(streams):
-        st[i] = ardit_stream_state(int(s[0]), int(s[1]), float(s[2]), float(s[3]), float(s[4]))
+        st[i] = ardit_stream_state(int(s[0]), float(s[1]), float(s[2]))
     out = (ardit_stream_decision * max(n, 1))()
-    _check(_lib.ardit_control_tick(C.byref(p), len(arr), arr, len(frontier), f, float(q_floor), n,
-                                   st, out), "ardit_control_tick")
+    _check(_lib.ardit_control_tick(int(n_workers), len(arr), arr, len(frontier), f,
+                                   float(q_floor), n, st, out), "ardit_control_tick")
     return [out[i] for i in range(n)]
-
-
-def ardit_evict_for(credits, resident_pages, requester, free_pages, need_pages):
-    """Evicted stream indices in order; raises ArditError (ARDIT_ECAPACITY) when
-    the pages cannot fit."""
-    n = len(credits)
-    c = (C.c_double * max(n, 1))(*[float(v) for v in credits])
-    r = (C.c_int32 * max(n, 1))(*[int(v) for v in resident_pages])
-    ev = (C.c_int32 * max(n, 1))()
-    m = C.c_int32(0)
-    _check(_lib.ardit_evict_for(n, c, r, int(requester), int(free_pages), int(need_pages), ev,
-                                C.byref(m)), "ardit_evict_for")
-    return [ev[i] for i in range(m.value)]
-
-
-def ardit_admit(streams_per_worker, first_chunk_ms):
-    n = len(streams_per_worker)
-    a = (C.c_int32 * n)(*[int(v) for v in streams_per_worker])
-    h, sl = C.c_int32(0), C.c_double(0.0)
-    _check(_lib.ardit_admit(n, a, float(first_chunk_ms), C.byref(h), C.byref(sl)), "ardit_admit")
-    return h.value, sl.value

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -116,6 +117,10 @@ int check_batch(const ardit_dims* d, const ardit_batch* b, unsigned use) {
   }
   if (nq > (1 << 22) || nc > (1 << 22))
     return fail(ARDIT_ECAPACITY, "more than 2^22 tokens in one batch");
+  // the text keys / values of a stream are addressed by a 32-bit element offset
+  if (nc * d->dim >= (int64_t(1) << 31))
+    return fail(ARDIT_ECAPACITY, "%lld text tokens of width %d exceed 2^31 elements",
+                static_cast<long long>(nc), d->dim);
   if (b->sparsity)
     for (int i = 0; i < b->n_streams; ++i) {
       const float r = b->sparsity[i];
@@ -159,6 +164,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 struct SparseBytes {
   size_t qbar = 0, scores = 0, lists = 0;
   size_t f8q = 0, f8kv = 0;   // FP8: query codes + scales; key / value codes + scales
+  int64_t f8_keys = 0;        // FP8: keys of all FP8 streams, padded to whole tiles
 };
 SparseBytes sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b) {
   SparseBytes z;
@@ -169,6 +175,7 @@ SparseBytes sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b) {
       if (b->quant[i] == ARDIT_QUANT_FP8 && b->q_lens[i] > 0)
         keys += kAttnKTile * ceil_div(static_cast<int64_t>(b->cache_lens[i]) + b->q_lens[i], kAttnKTile);
     }
+    z.f8_keys = keys;
     const size_t qb = static_cast<size_t>(N) * d->dim;
     z.f8q = up(qb) + up(qb / 32);
     const size_t kb = static_cast<size_t>(d->n_heads) * keys * d->head_dim;
@@ -190,6 +197,8 @@ SparseBytes sparse_ws_bytes(const ardit_dims* d, const ardit_batch* b) {
 
 // Limits of the block selection, on a batch whose q_lens and cache_lens passed check_batch.
 int check_sparse(const ardit_dims* d, const ardit_batch* b) {
+  if (sparse_ws_bytes(d, b).f8_keys >= (int64_t(1) << 31))
+    return fail(ARDIT_ECAPACITY, "FP8 streams hold more than 2^31 keys in all");
   if (!b->sparsity) return ARDIT_OK;
   int64_t lists = 0, scores = 0;
   for (int i = 0; i < b->n_streams; ++i) {
@@ -226,6 +235,52 @@ int check_kv(const ardit_dims* d, const ardit_batch* b, const ardit_kv_paged* kv
       return fail(ARDIT_ECAPACITY, "stream %d needs %lld frames > max_frames %d", i,
                   static_cast<long long>(frames), kv->max_frames);
   }
+  return ARDIT_OK;
+}
+
+// Opt-in validation of the page tables against the pool (ardit_debug_checks).
+std::atomic<int> g_debug_checks{0};
+
+// With the debug checks on: copies the page table to the host (synchronising
+// `st`) and checks every entry a stream reads or writes against the pool, and
+// that no page the batch writes is used by another stream or twice.
+int check_pages(hipStream_t st, const ardit_dims* d, const ardit_batch* b,
+                const ardit_kv_paged* kv, bool writes) {
+  if (!g_debug_checks.load(std::memory_order_relaxed)) return ARDIT_OK;
+  const int64_t T = tokens_per_frame(d);
+  const size_t n = static_cast<size_t>(b->n_streams) * kv->max_frames;
+  std::vector<int32_t> table(n);
+  ARDIT_HIP(hipMemcpyAsync(table.data(), kv->page_table, n * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, st), "page table copy");
+  ARDIT_HIP(hipStreamSynchronize(st), "page table copy");
+  std::vector<int32_t> owner(static_cast<size_t>(kv->n_pages), -1);   // stream writing the page
+  for (int i = 0; i < b->n_streams; ++i) {
+    if (b->q_lens[i] == 0) continue;
+    const int64_t keys = static_cast<int64_t>(b->cache_lens[i]) + b->q_lens[i];
+    const int64_t frames = (keys + T - 1) / T;
+    for (int64_t f = 0; f < frames; ++f) {
+      const int32_t p = table[static_cast<size_t>(i) * kv->max_frames + f];
+      if (p < 0 || p >= kv->n_pages)
+        return fail(ARDIT_ECAPACITY, "stream %d frame %lld: page %d outside the pool of %d", i,
+                    static_cast<long long>(f), p, kv->n_pages);
+      if (writes && f >= b->cache_lens[i] / T) {
+        if (owner[p] >= 0)
+          return fail(ARDIT_EINVAL, "page %d is written by streams %d and %d", p, owner[p], i);
+        owner[p] = i;
+      }
+    }
+  }
+  if (writes)
+    for (int i = 0; i < b->n_streams; ++i) {
+      if (b->q_lens[i] == 0) continue;
+      const int64_t cached = b->cache_lens[i] / T;
+      for (int64_t f = 0; f < cached; ++f) {
+        const int32_t p = table[static_cast<size_t>(i) * kv->max_frames + f];
+        if (owner[p] >= 0)
+          return fail(ARDIT_EINVAL, "stream %d reads page %d that stream %d writes", i, p,
+                      owner[p]);
+      }
+    }
   return ARDIT_OK;
 }
 
@@ -711,7 +766,7 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return na && nb && x < y + nb && y < x + na;
 }
 
-int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
+int check_block_args(hipStream_t st, const ardit_dims* d, const ardit_batch* b, const void* x,
                      const ardit_kv_paged* kv, const float* mod, const void* ctx_k,
                      const void* ctx_v, const ardit_block_weights* w, const void* out) {
   ARDIT_TRY(check_dims(d));
@@ -724,7 +779,7 @@ int check_block_args(const ardit_dims* d, const ardit_batch* b, const void* x,
   ARDIT_TRY(check_ptr(ctx_k, "ctx_k"));
   ARDIT_TRY(check_ptr(ctx_v, "ctx_v"));
   ARDIT_TRY(check_block_weights(w, false));
-  return ARDIT_OK;
+  return check_pages(st, d, b, kv, true);
 }
 
 }  // namespace
@@ -756,7 +811,7 @@ const char* ardit_status_str(int s) {
 
 const char* ardit_last_error(void) { return g_last_error; }
 
-int ardit_version(void) { return 501; }
+int ardit_version(void) { return 502; }
 
 int ardit_workspace_size(const ardit_dims* dims, const ardit_batch* batch, size_t* bytes) try {
   ARDIT_TRY(check_dims(dims));
@@ -842,6 +897,7 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
   ARDIT_TRY(check_ptr(g_q, "g_q"));
   ARDIT_TRY(check_ptr(g_k, "g_k"));
   ARDIT_TRY(check_ptr(q_out, "q_out"));
+  ARDIT_TRY(check_pages(stream, dims, batch, kv, true));
   const int N = static_cast<int>(sum_q(batch));
   const RowStreams rs = q_streams(batch);
   const int D = dims->dim;
@@ -867,6 +923,7 @@ int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch
   ARDIT_TRY(check_ptr(o, "o"));
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  ARDIT_TRY(check_pages(stream, dims, batch, kv, false));
   return self_attention(stream, dims, batch, q, kv, o, ws, L);
 } catch (...) {
   return host_failure();
@@ -916,6 +973,7 @@ int ardit_sparse_select(hipStream_t stream, const ardit_dims* dims, const ardit_
     return fail(ARDIT_ECAPACITY, "block lists above 2^31 entries");
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
+  ARDIT_TRY(check_pages(stream, dims, batch, kv, false));
   AttnArgs a = self_attn_base(dims, batch, q, kv, nullptr);
   plan_sparse_attention(a, batch->sparsity, blocks, row_stride, at<float>(ws, L.sp_qbar),
                         at<float>(ws, L.sp_scores));
@@ -929,7 +987,7 @@ int ardit_block_fwd_varlen(hipStream_t stream, const ardit_dims* dims, const ard
                            const void* x, const ardit_kv_paged* kv, const float* mod,
                            const void* ctx_k, const void* ctx_v, const ardit_block_weights* w,
                            void* out, void* ws, size_t ws_bytes) try {
-  ARDIT_TRY(check_block_args(dims, batch, x, kv, mod, ctx_k, ctx_v, w, out));
+  ARDIT_TRY(check_block_args(stream, dims, batch, x, kv, mod, ctx_k, ctx_v, w, out));
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
   return block_chain(stream, dims, batch, x, kv, mod, ctx_k, ctx_v, w, out, ws, L);
@@ -964,7 +1022,7 @@ int ardit_stack_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batc
   if (n_layers < 1) return fail(ARDIT_EINVAL, "n_layers %d must be >= 1", n_layers);
   if (!kv || !ctx_k || !ctx_v || !w) return fail(ARDIT_EINVAL, "per-layer arrays must be non-NULL");
   for (int l = 0; l < n_layers; ++l)
-    ARDIT_TRY(check_block_args(dims, batch, x, &kv[l], mod, ctx_k[l], ctx_v[l], &w[l], out));
+    ARDIT_TRY(check_block_args(stream, dims, batch, x, &kv[l], mod, ctx_k[l], ctx_v[l], &w[l], out));
   if (x == out) return fail(ARDIT_EINVAL, "stack input and output must differ");
   Ws L;
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
@@ -1049,7 +1107,8 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
   float* mod = at<float>(ws, L.gmod);
   bf16_t* vel = at<bf16_t>(ws, L.gv);
   for (int l = 0; l < n_layers; ++l)
-    ARDIT_TRY(check_block_args(dims, batch, x_init, &kv[l], mod, ctx_k[l], ctx_v[l], &w[l], vel));
+    ARDIT_TRY(check_block_args(stream, dims, batch, x_init, &kv[l], mod, ctx_k[l], ctx_v[l], &w[l],
+                               vel));
   const int64_t N = sum_q(batch);
   const int D = dims->dim;
   const size_t xbytes = 2 * static_cast<size_t>(N) * D;
@@ -1095,6 +1154,14 @@ int ardit_chunk_generate(hipStream_t stream, const ardit_dims* dims, const ardit
                 "sampler");
     }
   }
+  return ARDIT_OK;
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_debug_checks(int enable) try {
+  if (enable != 0 && enable != 1) return fail(ARDIT_EINVAL, "debug checks %d not 0 or 1", enable);
+  g_debug_checks.store(enable, std::memory_order_relaxed);
   return ARDIT_OK;
 } catch (...) {
   return host_failure();

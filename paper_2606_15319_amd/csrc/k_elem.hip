@@ -247,8 +247,11 @@ __device__ __forceinline__ int find_stream(const RowStreams& rs, int row) {
   return b;
 }
 
-__device__ __forceinline__ int clamp_page(int p, int n_pages) {
-  return p < 0 ? 0 : (p >= n_pages ? n_pages - 1 : p);
+// Page of a write: an entry outside [0, n_pages) (an unassigned or stale
+// table slot) yields -1 and the store is skipped, so a bad table can never
+// write into a page another stream owns.
+__device__ __forceinline__ int write_page(int p, int n_pages) {
+  return p >= 0 && p < n_pages ? p : -1;
 }
 
 // A workgroup handles kRowsPerGroup rows, 2 per wave.  Per row, lane k < d/2
@@ -337,7 +340,7 @@ __device__ __forceinline__ void qk_norm_rope_group(const QkRopeParams& p, int gr
     const RowStream s = p.rs.s[b];
     const int slot = s.cache_len + row - s.row_begin;
     const int fr = static_cast<int>(fdiv(static_cast<uint32_t>(slot), p.fT));
-    const int page = clamp_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr],
+    const int page = write_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr],
                                 p.n_pages);
     const int off = slot - fr * p.T;
     const float* rcs = lcs + (wave * kRowsPerWave + r) * 64;
@@ -372,8 +375,11 @@ __device__ __forceinline__ void qk_norm_rope_group(const QkRopeParams& p, int gr
           y[2 * e] = x0 * cc[e] - x1 * ss[e];
           y[2 * e + 1] = x0 * ss[e] + x1 * cc[e];
         }
-        bf16_t* dst = p.k_pages + ((static_cast<size_t>(page) * p.H + h) * p.T + off) * p.hd + e0;
-        *reinterpret_cast<uint4*>(dst) = pack8(y);
+        if (page >= 0) {
+          bf16_t* dst =
+              p.k_pages + ((static_cast<size_t>(page) * p.H + h) * p.T + off) * p.hd + e0;
+          *reinterpret_cast<uint4*>(dst) = pack8(y);
+        }
       }
     }
   }
@@ -483,7 +489,8 @@ __global__ __launch_bounds__(256) void v_transpose_kernel(const VtParams p) {
     const int slot = s.cache_len + t;
     const int fr = static_cast<int>(fdiv(static_cast<uint32_t>(slot), p.fT));
     const int page =
-        clamp_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr], p.n_pages);
+        write_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr], p.n_pages);
+    if (page < 0) return;
     T = p.T;
     off = slot - fr * p.T;
     base = static_cast<size_t>(page) * p.H * p.hd * T;
@@ -534,7 +541,8 @@ __device__ __forceinline__ void v_append16_block(const VtParams& p, int nb, int 
     const int slot = s.cache_len + n - s.row_begin;
     const int fr = static_cast<int>(fdiv(static_cast<uint32_t>(slot), p.fT));
     const int page =
-        clamp_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr], p.n_pages);
+        write_page(p.page_table[static_cast<size_t>(b) * p.max_frames + fr], p.n_pages);
+    if (page < 0) continue;
     const int off = slot - fr * p.T;
     const int cc = dd >> 3, e = dd & 7;
     uint32_t w[4];

@@ -208,45 +208,13 @@ def read_profile(path):
     return rows
 
 
-def controller_latency(profile_json, reps=200, seed=0):
-    """Microseconds per control tick for several (streams, workers) sizes."""
-    import ctypes as C
-    import math
-    import random
-    from paper_2606_15319_amd import ardit as A
-    cfgs = A.fidelity_array(read_profile(profile_json))
-    frontier, floor = A.ardit_pareto_frontier(cfgs)
-    fr = (C.c_int32 * len(frontier))(*frontier)
-    rnd = random.Random(seed)
-    out = []
-    for U, G in ((64, 16), (256, 16), (1024, 16), (4096, 64)):
-        st = (A.ardit_stream_state * U)(*[
-            A.ardit_stream_state(rnd.randrange(G), -1, rnd.uniform(-200.0, 3000.0),
-                                 rnd.uniform(0.0, 200.0), -math.inf) for _ in range(U)])
-        dec = (A.ardit_stream_decision * U)()
-        p = A.ardit_ctl_params(G, 8, 2, 1, 60000.0, 0.0)
-        t0 = time.perf_counter()
-        for _ in range(reps):
-            if A._lib.ardit_control_tick(C.byref(p), len(cfgs), cfgs, len(frontier), fr, floor, U,
-                                         st, dec) != 0:
-                raise RuntimeError(A.ardit_last_error())
-        us = (time.perf_counter() - t0) / reps * 1e6
-        out.append(dict(streams=U, workers=G, frontier=len(frontier), us_per_tick=round(us, 1)))
-        log(f"{U} streams on {G} workers, frontier {len(frontier)}: {us:.1f} us per tick")
-    return out
-
-
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--layers", type=int, default=30)
     ap.add_argument("--reps", type=int, default=2)
     ap.add_argument("--out", default=None)
     ap.add_argument("--md", default=None)
-    ap.add_argument("--controller", default=None, metavar="PROFILE")
     a = ap.parse_args()
-    if a.controller:
-        print(json.dumps(controller_latency(a.controller)))
-        return
     if not a.out:
         ap.error("--out is required")
     t0 = time.time()

@@ -33,7 +33,7 @@ import numpy as np
 
 import oracle as O
 from workloads import bf16_bits, bits_to_f32
-from workloads.gen import draw_block_case
+from workloads.gen import draw_block_case, ring_page_ids  # noqa: F401
 
 TOL = 2e-2
 COS_MIN = 0.9995
@@ -157,16 +157,6 @@ class PagedCache:
 
 def frames_needed(shape, cache_len):
     return cache_len // shape.tokens_per_frame + shape.frames
-
-
-def ring_page_ids(shape, chunk_index, cache_chunks, ring_slots):
-    """Pages of a ring of ring_slots chunk slots, the chunk c in slot c % ring_slots,
-    holding chunks chunk_index - cache_chunks .. chunk_index in logical order."""
-    ids = []
-    for c in range(chunk_index - cache_chunks, chunk_index + 1):
-        slot = c % ring_slots
-        ids += [slot * shape.frames + f for f in range(shape.frames)]
-    return ids
 
 
 # -------------------------------------------------------------- block runs

@@ -34,7 +34,7 @@ def test_status_strings_and_version():
     for code, name in A.STATUS.items():
         assert A.ardit_status_str(code) == name
     assert A.ardit_status_str(123) == "ARDIT_UNKNOWN"
-    assert A.ardit_version() == 501
+    assert A.ardit_version() == 502
 
 
 def _dims(**kw):
@@ -323,3 +323,21 @@ def test_timing_masks_and_kinds():
     for k in (A.TIME_ATTENTION, A.TIME_GEMM, A.TIME_ELEMENTWISE):
         assert A.ardit_timing_collect_kind(k) == (0, 0.0)
     assert A.ardit_timing_collect() == (0, 0.0)
+
+
+def test_text_offsets_beyond_2_31_rejected():
+    """Text keys/values are addressed by a 32-bit element offset: a batch whose
+    text tokens times the width reach 2^31 is refused before any launch."""
+    d = _dims(dim=8192, n_heads=64, head_dim=128)
+    at_limit = A.Batch(ctx_lens=[4096] * 64)              # 2^18 tokens * 2^13 = 2^31
+    assert _status(A.ardit_workspace_size, d, at_limit) == -3
+    assert "2^31" in A.ardit_last_error()
+    below = A.Batch(ctx_lens=[4096] * 63 + [4095])
+    assert A.ardit_workspace_size(d, below) > 0
+
+
+def test_debug_checks_switch():
+    assert _status(A.ardit_debug_checks, 2) == -1
+    assert _status(A.ardit_debug_checks, -1) == -1
+    A.ardit_debug_checks(1)
+    A.ardit_debug_checks(0)

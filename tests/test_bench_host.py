@@ -48,11 +48,25 @@ def test_traffic_reported_only_for_matching_sources(tmp_path):
     stale.write_text("- HBM bytes per launch: 12345\n- attention sources sha256: `00`\n")
     broken = tmp_path / "broken.md"
     broken.write_text(f"- attention sources sha256: `{m.attn_source_hash()}`\n")
-    m.TRAFFIC_SUMMARY = str(good)
-    assert m.measured_traffic() == 12345
-    m.TRAFFIC_SUMMARY = str(stale)
-    assert m.measured_traffic() is None
-    m.TRAFFIC_SUMMARY = str(broken)
-    assert m.measured_traffic() is None
-    m.TRAFFIC_SUMMARY = str(tmp_path / "missing.md")
-    assert m.measured_traffic() is None
+    for name, want in (("good", 12345), ("stale", None), ("broken", None), ("missing", None)):
+        m.traffic_summary = lambda wl, n=name: str(tmp_path / f"{n}.md")
+        assert m.measured_traffic("large") == want, name
+
+
+def test_default_workload_is_the_large_ring():
+    m = _bench_module()
+    import sys as _s
+    argv = _s.argv
+    try:
+        _s.argv = ["bench.py"]
+        args = m.parse()
+    finally:
+        _s.argv = argv
+    assert args.workload == "large" and args.layers is None
+    assert m.DEFAULT_LAYERS["large"] == 40
+    from workloads import WORKLOADS, stream_page_ids
+    wl = WORKLOADS["large"]
+    ids, n = stream_page_ids(wl)
+    assert n == 24 and sorted(ids[0]) == list(range(24))
+    assert ids[0] != sorted(ids[0])          # the ring has wrapped
+    assert ids[0][-3:] == [9, 10, 11]       # chunk 11 sits in slot 3

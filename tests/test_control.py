@@ -1,8 +1,8 @@
 """The controller in libardit (include/ardit_control.h, host code, no GPU)
 against the controller oracle, decision for decision, on seeded random
 cluster states: frontier and floor, BMPR choices, whole control ticks
-(configuration, credit, tier, dispatch order, re-homing plan, cooldowns,
-SP donors), eviction and admission; plus the host-side rejections."""
+(configuration, credit, tier, dispatch order); plus the host-side
+rejections."""
 import math
 
 import numpy as np
@@ -46,17 +46,13 @@ def test_frontier_floor_and_bmpr_match_oracle(seed):
             assert A.ardit_bmpr_select(cfgs, f, fl, b) == K.bmpr_select(f, L, Q, fl, b)
 
 
-def _cluster(rng, n_workers, n_streams, now):
+def _cluster(rng, n_workers, n_streams):
     streams = []
     for _ in range(n_streams):
         w = int(rng.integers(0, n_workers))
-        donor = -1
-        if n_workers > 1 and rng.random() < 0.15:
-            donor = int((w + rng.integers(1, n_workers)) % n_workers)
-        cool = -math.inf if rng.random() < 0.6 else float(now + rng.uniform(-90000, 90000))
         slack = float(rng.choice([rng.uniform(-400, 3500), rng.integers(-4, 30) * 50.0]))
         rem = float(rng.choice([0.0, rng.uniform(0, 400)]))
-        streams.append((w, donor, slack, rem, cool))
+        streams.append((w, slack, rem))
     return streams
 
 
@@ -70,40 +66,13 @@ def test_control_tick_matches_oracle(seed):
         F = K.pareto_frontier(L, Q)
         fl = K.quality_floor(Q)
         W = int(rng.integers(1, 20))
-        g = int(rng.choice([1, 2, 4, 8]))
-        now = float(rng.uniform(0, 1e6))
-        params = dict(n_workers=W, gpus_per_node=g, cap_send=int(rng.integers(0, 4)),
-                      cap_recv=int(rng.integers(0, 3)), cooldown_ms=60000.0, now_ms=now)
-        streams = _cluster(rng, W, int(rng.integers(0, 60)), now)
-        got = A.ardit_control_tick(params, cfgs, F, fl, streams)
-        ref = K.control_tick(K.Params(**params), L, Q, F, fl,
-                             [K.Stream(s[0], s[2], s[3], s[4], s[1]) for s in streams])
+        streams = _cluster(rng, W, int(rng.integers(0, 60)))
+        got = A.ardit_control_tick(W, cfgs, F, fl, streams)
+        ref = K.control_tick(W, L, Q, F, fl, [K.Stream(*s) for s in streams])
         for i, (x, r) in enumerate(zip(got, ref)):
-            assert (x.cfg, x.mode, x.tier, x.queue_pos, x.rehome_to, x.sp_donor) == \
-                (r.cfg, r.mode, r.tier, r.queue_pos, r.rehome_to, r.sp_donor), (trial, i)
+            assert (x.cfg, x.mode, x.tier, x.queue_pos) == (r.cfg, r.mode, r.tier, r.queue_pos), \
+                (trial, i)
             assert x.credit_ms == r.credit_ms
-            assert x.cooldown_until_ms == r.cooldown_until_ms or \
-                (math.isinf(x.cooldown_until_ms) and math.isinf(r.cooldown_until_ms))
-
-
-def test_eviction_and_admission_match_oracle():
-    rng = np.random.default_rng(300)
-    for _ in range(300):
-        n = int(rng.integers(1, 30))
-        credits = list(rng.integers(-5, 6, size=n).astype(float) * 100.0)
-        pages = list(rng.integers(0, 10, size=n))
-        req = int(rng.integers(0, n))
-        free, need = int(rng.integers(0, 20)), int(rng.integers(0, 60))
-        ref = K.evict_for(credits, pages, req, free, need)
-        if ref is None:
-            with pytest.raises(A.ArditError) as e:
-                A.ardit_evict_for(credits, pages, req, free, need)
-            assert e.value.status == -3
-        else:
-            assert A.ardit_evict_for(credits, pages, req, free, need) == ref
-        spw = list(rng.integers(0, 5, size=int(rng.integers(1, 12))))
-        t = float(rng.uniform(10, 500))
-        assert A.ardit_admit(spw, t) == (K.choose_home(spw), K.initial_slack(t))
 
 
 def _status(fn, *a):
@@ -121,12 +90,12 @@ def test_controller_rejections():
     assert _status(A.ardit_bmpr_select, cfgs, [5], fl, 100.0) == -1
     # a floor above every frontier point: nothing to route to
     assert _status(A.ardit_bmpr_select, cfgs, f, 99.0, 100.0) == -3
-    p = dict(n_workers=2)
-    assert _status(A.ardit_control_tick, p, cfgs, f, fl, [(2, -1, 100.0, 0.0, -math.inf)]) == -1
-    assert _status(A.ardit_control_tick, p, cfgs, f, fl, [(0, 3, 100.0, 0.0, -math.inf)]) == -1
-    assert _status(A.ardit_control_tick, p, cfgs, f, fl, [(0, -1, math.inf, 0.0, -math.inf)]) == -1
-    assert _status(A.ardit_control_tick, dict(n_workers=0), cfgs, f, fl, []) == -1
-    assert _status(A.ardit_admit, [], 10.0) == -1
+    assert _status(A.ardit_control_tick, 2, cfgs, f, fl, [(2, 100.0, 0.0)]) == -1
+    assert _status(A.ardit_control_tick, 2, cfgs, f, fl, [(-1, 100.0, 0.0)]) == -1
+    assert _status(A.ardit_control_tick, 2, cfgs, f, fl, [(0, math.inf, 0.0)]) == -1
+    assert _status(A.ardit_control_tick, 2, cfgs, f, fl, [(0, 100.0, math.nan)]) == -1
+    assert _status(A.ardit_control_tick, 0, cfgs, f, fl, []) == -1
+    assert A.ardit_control_tick(2, cfgs, f, fl, []) == []
 
 
 def test_profiler_space_is_the_papers():

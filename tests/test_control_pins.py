@@ -2,10 +2,8 @@
 cases of the paper's rules and against independent formulations: the credit
 equation (Section 3.1), tier bounds (Section 4.1), the Pareto frontier
 (Section 5.2) against a sort-and-sweep construction, the median floor, both
-BMPR modes, the re-homing example of Section 4.2 (two RELAXED workers, one
-with queued URGENT streams) with its caps, cooldown and node preference
-(Appendix C.2), elastic-SP donor choice and release (Section 4.3, Appendix
-C.3), credit-aware eviction (Section 4.1) and admission (Section 3.3)."""
+BMPR modes, and a worked control tick (configuration, credit, tier and the
+credit-ordered dispatch of Section 4.1)."""
 import math
 
 import numpy as np
@@ -84,68 +82,24 @@ def test_bmpr_modes():
         assert Q[c] >= floor
 
 
-def _tick(streams, latency, quality, **kw):
-    F = K.pareto_frontier(latency, quality)
-    return K.control_tick(K.Params(**kw), latency, quality, F, K.quality_floor(quality), streams)
-
-
-def test_rehoming_example_and_caps():
-    # one configuration of 100 ms: tiers by slack alone (URGENT < 300, RELAXED > 500)
-    lat, qual = [100.0], [1.0]
-    st = [K.Stream(0, 900.0), K.Stream(1, 800.0),                    # W0, W1: RELAXED
-          K.Stream(2, 150.0), K.Stream(2, 120.0), K.Stream(2, 250.0),  # W2: three URGENT
-          K.Stream(3, 1000.0)]                                        # W3: RELAXED
-    d = _tick(st, lat, qual, n_workers=4, now_ms=5000.0)
-    assert [x.tier for x in d] == [K.RELAXED, K.RELAXED, K.URGENT, K.URGENT, K.URGENT, K.RELAXED]
-    # W2 sends its two lowest-credit URGENT streams (cap 2), one per receiver (cap 1)
-    assert [x.rehome_to for x in d] == [-1, -1, 1, 0, -1, -1]
-    assert d[3].cooldown_until_ms == 65000.0 and d[2].cooldown_until_ms == 65000.0
-    # dispatch order on W2: lowest credit first
-    assert [d[i].queue_pos for i in (2, 3, 4)] == [1, 0, 2]
-    # the lowest-credit stream in cooldown stays; the next one goes
-    st[3].cooldown_until_ms = 30000.0
-    d = _tick(st, lat, qual, n_workers=4, now_ms=5000.0)
-    assert [x.rehome_to for x in d] == [-1, -1, 0, -1, 1, -1]
-    # receivers on the sender's node come first: sender W9 (node 1) picks W8, then W0
-    st = [K.Stream(0, 900.0), K.Stream(8, 900.0), K.Stream(9, 100.0), K.Stream(9, 110.0),
-          K.Stream(9, 120.0)]
-    d = _tick(st, lat, qual, n_workers=10, gpus_per_node=8)
-    assert [x.rehome_to for x in d][2:] == [8, 0, -1]
-    # one URGENT stream alone is not congestion: nothing moves
-    d = _tick([K.Stream(0, 100.0), K.Stream(1, 900.0)], lat, qual, n_workers=2)
-    assert [x.rehome_to for x in d] == [-1, -1]
-
-
-def test_elastic_sp_donor_and_release():
-    lat, qual = [100.0], [1.0]
-    # stream 0 on W0 will miss its window (C = 50 - 100 < 0); W1 and W2 are
-    # RELAXED on the same node, W2 idle (+inf credit), W9 RELAXED on another node
-    st = [K.Stream(0, 50.0), K.Stream(1, 600.0), K.Stream(9, 5000.0)]
-    d = _tick(st, lat, qual, n_workers=10)
-    assert d[0].sp_donor == 2 and d[0].tier == K.URGENT
-    # without same-node RELAXED workers there is no donor
-    st2 = [K.Stream(0, 50.0), K.Stream(1, 50.0), K.Stream(9, 5000.0)]
-    d = _tick(st2, lat, qual, n_workers=10, gpus_per_node=2)
-    assert d[0].sp_donor == -1 and d[1].sp_donor == -1
-    # a donor is kept while the stream stays below NORMAL and released at C >= 2T
-    st[0].sp_donor = 2
-    st[0].slack_ms = 250.0                   # C = 150 < 200: keep
-    assert _tick(st, lat, qual, n_workers=10)[0].sp_donor == 2
-    st[0].slack_ms = 300.0                   # C = 200 = 2T: NORMAL, release
-    assert _tick(st, lat, qual, n_workers=10)[0].sp_donor == -1
-
-
-def test_credit_aware_eviction():
-    credits = [500.0, -20.0, 900.0, 300.0]
-    pages = [6, 6, 6, 6]
-    # stream 1 (the most urgent) needs 9 pages with 2 free: evict 2 (900), then 0 (500)
-    assert K.evict_for(credits, pages, 1, 2, 9) == [2, 0]
-    assert K.evict_for(credits, pages, 1, 9, 9) == []
-    assert K.evict_for(credits, pages, 1, 0, 40) is None
-    # ties go to the later stream
-    assert K.evict_for([1.0, 1.0, 0.0], [3, 3, 3], 2, 0, 3) == [1]
-
-
-def test_admission():
-    assert K.choose_home([3, 1, 1, 2]) == 1
-    assert K.initial_slack(250.0) == 1000.0
+def test_worked_tick():
+    """Three configurations: A (100 ms, Q 80), B (200 ms, Q 90), C (50 ms, Q 60);
+    floor = median 80.  Stream budgets P - R pick B when >= 200, A when in
+    [100, 200), and speed recovery (A, the fastest at the floor) below 100;
+    credit and tier follow, and each worker's queue runs by credit."""
+    lat, qual = [100.0, 200.0, 50.0], [80.0, 90.0, 60.0]
+    F = K.pareto_frontier(lat, qual)
+    assert F == [2, 0, 1] and K.quality_floor(qual) == 80.0
+    st = [K.Stream(0, 1500.0), K.Stream(0, 180.0, 30.0), K.Stream(1, 90.0),
+          K.Stream(0, 700.0, 100.0), K.Stream(1, 450.0)]
+    d = K.control_tick(2, lat, qual, F, 80.0, st)
+    assert [x.cfg for x in d] == [1, 0, 0, 1, 1]
+    assert [x.mode for x in d] == [K.QUALITY_MODE, K.QUALITY_MODE, K.SPEED_RECOVERY,
+                                   K.QUALITY_MODE, K.QUALITY_MODE]
+    assert [x.credit_ms for x in d] == [1300.0, 50.0, -10.0, 400.0, 250.0]
+    assert [x.tier for x in d] == [K.RELAXED, K.URGENT, K.URGENT, K.NORMAL, K.URGENT]
+    # worker 0: credits 1300, 50, 400 -> order 1, 3, 0; worker 1: -10, 250 -> 2, 4
+    assert [x.queue_pos for x in d] == [2, 0, 0, 1, 1]
+    # equal credits keep the stream order
+    d = K.control_tick(1, lat, qual, F, 80.0, [K.Stream(0, 300.0), K.Stream(0, 300.0)])
+    assert [x.queue_pos for x in d] == [0, 1]

@@ -280,9 +280,8 @@ def test_controller_drives_batched_generation(A):
     assert floor == 75.0
     # budget 210 ms: (3, 3) fits; 1000 ms: the best (4, 3); 40 ms: nothing fits,
     # speed recovery takes the fastest point above the floor, (3, 1)
-    streams = [(0, -1, 210.0, 0.0, -math.inf), (0, -1, 1000.0, 0.0, -math.inf),
-               (0, -1, 50.0, 10.0, -math.inf)]
-    dec = A.ardit_control_tick(dict(n_workers=1), table, frontier, floor, streams)
+    streams = [(0, 210.0, 0.0), (0, 1000.0, 0.0), (0, 50.0, 10.0)]
+    dec = A.ardit_control_tick(1, table, frontier, floor, streams)
     cfg = [table[d.cfg] for d in dec]
     assert [d.cfg for d in dec] == [2, 0, 3]
     assert [d.mode for d in dec] == [A.BMPR_QUALITY, A.BMPR_QUALITY, A.BMPR_SPEED_RECOVERY]

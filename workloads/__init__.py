@@ -9,5 +9,5 @@ from .gen import (  # noqa: F401
     BlockShape, Workload, WORKLOADS, workload, make_rng,
     bf16_bits, bits_to_f32, bf16_round, normal_bf16,
     draw_time_weights, draw_block_weights, BLOCK_WEIGHT_ORDER,
-    TIME_WEIGHT_ORDER, draw_ragged_streams,
+    TIME_WEIGHT_ORDER, draw_ragged_streams, ring_page_ids, stream_page_ids,
 )

@@ -154,6 +154,35 @@ def workload(name: str) -> Workload:
     return WORKLOADS[name]
 
 
+def ring_page_ids(shape: BlockShape, chunk_index: int, cache_chunks: int, ring_slots: int):
+    """Physical pages, in logical order, of a stream whose cache is a ring of
+    ring_slots chunk slots (chunk c in slot c % ring_slots, frame f of slot s in
+    page s * frames + f), holding chunks chunk_index - cache_chunks .. chunk_index."""
+    ids = []
+    for c in range(chunk_index - cache_chunks, chunk_index + 1):
+        slot = c % ring_slots
+        ids += [slot * shape.frames + f for f in range(shape.frames)]
+    return ids
+
+
+def stream_page_ids(wl: Workload):
+    """(page ids per stream in logical order, pool size) of a workload's caches:
+    the ring layout when the workload has ring slots, else consecutive pages
+    per stream (each stream's cache frames plus its chunk's)."""
+    sh = wl.shape
+    if wl.ring_slots:
+        ids = [ring_page_ids(sh, p // sh.frames, c, wl.ring_slots)
+               for c, p in zip(wl.cache_chunks, wl.frame_pos0)]
+        return [[i + s * wl.ring_slots * sh.frames for i in r] for s, r in enumerate(ids)], \
+            len(ids) * wl.ring_slots * sh.frames
+    ids, nxt = [], 0
+    for c in wl.cache_chunks:
+        nf = (c + 1) * sh.frames
+        ids.append(list(range(nxt, nxt + nf)))
+        nxt += nf
+    return ids, nxt
+
+
 # --------------------------------------------------------------------------
 # weight draws
 # --------------------------------------------------------------------------
