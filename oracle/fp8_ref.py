@@ -24,11 +24,17 @@ format or granularity; this module takes these readings:
 `fp8_attention` returns the attention of the dequantised q8, k8, v8 with
 exact (unquantised) weights, together with an element-wise bound on what
 quantising the weights, and the kernels' fp32 arithmetic, may add (see
-`weight_quant_bound`).  Pins (tests/test_oracle_pins.py): every E4M3 code
-rounds to itself, midpoints round to even, the block exponent and the
+`weight_quant_bound`), and the standard deviation that rounding the weights
+gives each output element (`weight_quant_sigma`): the worst case grows with
+the sum of |v| under the weights, the spread only with their root sum of
+squares, which is what an output element itself scales with.  Pins
+(tests/test_oracle_pins.py): every E4M3 code rounds to itself, midpoints round to even, the block exponent and the
 [128, 256) landing of the block maximum, power-of-two scale invariance,
 error within half a quantum, exactly representable inputs pass unchanged,
-and weight quantisation stays within the bound on random inputs.
+weight quantisation stays within the bound on random inputs, and the
+statistical criterion built on sigma (tests/harness.py, fp8_parity) accepts
+quantised weights at 14040 and 32760 keys while rejecting an all-zero
+output, half the output and a 2% scale error.
 """
 from __future__ import annotations
 
@@ -126,16 +132,42 @@ def weight_quant_bound(p, v8, l):
     return (per @ np.abs(v8)) / l[:, None]
 
 
-def fp8_attention(q, k, v, mask=None):
-    """FP8 attention of one stream: returns (o [Lq, H, d], bound [Lq, H, d]).
+def weight_quant_sigma(p, v8, l):
+    """Standard deviation of sum_j (p8_j - p_j) v_jd / l for one head when each
+    weight's rounding error is uniform within half its E4M3 quantum and
+    independent of the others (round to nearest of values spread over many
+    quanta).  p, v8, l as for weight_quant_bound; the quantum of weight j is
+    that of p_j / 2^e in E4M3 times 2^e, e the exponent of its block of 32
+    keys (block_exponent of the block's largest weight): 2^(E - 3) for
+    E = floor(log2(p_j / 2^e)) >= -6, else 2^-9.  Variance quantum^2 / 12."""
+    R, Lk = p.shape
+    nb = (Lk + BLOCK - 1) // BLOCK
+    pad = nb * BLOCK - Lk
+    pb = np.concatenate([p, np.zeros((R, pad))], axis=1).reshape(R, nb, BLOCK)
+    e = np.repeat(block_exponent(pb.max(axis=2)), BLOCK, axis=1)[:, :Lk]
+    y = p / np.ldexp(1.0, e)
+    _, ex = np.frexp(np.where(y > 0, y, 1.0))        # y = f 2^ex, f in [0.5, 1)
+    E = np.where(y > 0, np.maximum(ex - 1, -6), -6)
+    quantum = np.ldexp(1.0, E - 3 + e)
+    var = quantum * quantum / 12.0
+    return np.sqrt(var @ (v8 * v8)) / l[:, None]
+
+
+def fp8_attention(q, k, v, mask=None, sigma=False):
+    """FP8 attention of one stream: returns (o [Lq, H, d], bound [Lq, H, d]),
+    and with sigma=True also sigma [Lq, H, d].
 
     o is softmax(q8 k8^T / sqrt(d)) v8 in float64 with the dequantised
-    operands and unquantised weights; bound is weight_quant_bound per head.
-    mask: optional [H, Lq, Lk] or [Lq, Lk] visibility (block-sparse use)."""
+    operands and unquantised weights; bound is weight_quant_bound per head (a
+    worst case: every weight rounded by its largest error in one direction);
+    sigma is weight_quant_sigma per head (the spread that rounding the weights
+    to E4M3 gives an output element).  mask: optional [H, Lq, Lk] or [Lq, Lk]
+    visibility (block-sparse use)."""
     q8, k8, v8 = quantize_qkv(q, k, v)
     Lq, H, d = q8.shape
     o = np.empty((Lq, H, d))
     bound = np.empty((Lq, H, d))
+    sig = np.empty((Lq, H, d)) if sigma else None
     scale = 1.0 / math.sqrt(d)
     for h in range(H):
         s = (q8[:, h] @ k8[:, h].T) * scale
@@ -146,7 +178,9 @@ def fp8_attention(q, k, v, mask=None):
         l = p.sum(axis=1)
         o[:, h] = (p @ v8[:, h]) / l[:, None]
         bound[:, h] = weight_quant_bound(p, v8[:, h], l)
-    return o, bound
+        if sigma:
+            sig[:, h] = weight_quant_sigma(p, v8[:, h], l)
+    return (o, bound, sig) if sigma else (o, bound)
 
 
 def fp8_attention_quantized_weights(q, k, v):

@@ -32,8 +32,8 @@ from __future__ import annotations
 import numpy as np
 
 import oracle as O
-from workloads import bf16_bits, bits_to_f32
-from workloads.gen import draw_block_case, ring_page_ids  # noqa: F401
+from workloads import bf16_bits, bits_to_f32, stream_page_ids
+from workloads.gen import GAIN_NAMES, block_weight_shapes, draw_block_case, ring_page_ids  # noqa: F401
 
 TOL = 2e-2
 COS_MIN = 0.9995
@@ -107,6 +107,37 @@ def parity(gpu, ref, name, tol=TOL, cos_min=COS_MIN, quantum=None, half_ulps=1.0
     return msg
 
 
+def fp8_parity(gpu, o_ref, sigma, name, z_rms_max=1.5, z_max=8.0, slope_max=5e-3,
+               cos_min=0.999):
+    """Parity of an FP8 attention output with the float64 FP8 oracle (exact
+    weights over the dequantised q8, k8, v8).  The one rounding the oracle
+    leaves out is that of the softmax weights to E4M3 (and the final bf16
+    store): each output element then carries an error of spread
+    s = sqrt(sigma^2 + half_ulp(o)^2 / 3), sigma from
+    fp8_ref.weight_quant_sigma, about 2.5% of |o| at any number of keys.
+    Asserted: the errors in units of s have an RMS <= z_rms_max and no element
+    beyond z_max (they are sums of many independent roundings); the error
+    has no component along o, |sum(err o)| / sum(o^2) <= slope_max (a scale
+    error of the output, which the spread alone would hide); and
+    cos(gpu, o_ref) >= cos_min."""
+    g = np.asarray(gpu, np.float64).ravel()
+    r = np.asarray(o_ref, np.float64).ravel()
+    assert np.isfinite(g).all(), f"{name}: non-finite GPU values"
+    hu = half_ulp_bf16(r)
+    s = np.sqrt(np.asarray(sigma, np.float64).ravel() ** 2 + hu * hu / 3.0) + 1e-30
+    err = g - r
+    z = err / s
+    z_rms = float(np.sqrt(np.mean(z * z)))
+    z_top = float(np.max(np.abs(z)))
+    slope = float(np.dot(err, r) / np.dot(r, r))
+    cos = float(np.dot(g, r) / (np.linalg.norm(g) * np.linalg.norm(r) + 1e-300))
+    msg = (f"{name}: z_rms={z_rms:.3f} z_max={z_top:.2f} slope={slope:.2e} cos={cos:.6f} "
+           f"rms(err)/rms(o)={float(np.sqrt(np.mean(err ** 2) / np.mean(r ** 2))):.4f}")
+    assert z_rms <= z_rms_max and z_top <= z_max and abs(slope) <= slope_max \
+        and cos >= cos_min, msg
+    return msg
+
+
 # -------------------------------------------------------------------- pages
 class PagedCache:
     """A device page pool for one layer plus the host view of its contents."""
@@ -153,6 +184,21 @@ class PagedCache:
     def device_bits(self):
         return (host_bits(self.k).reshape(self.k_host.shape),
                 host_bits(self.v).reshape(self.v_host.shape))
+
+
+def read_stream_pages(k_pages, v_pages, page_ids, n_tokens):
+    """Logical [n, H, d] keys and values (fp32, bf16-exact) of one stream read
+    back from device pools k_pages [P][H][T][d] and v_pages [P][H][d][T]
+    through its page ids (only the stream's pages are copied)."""
+    import torch
+    from paper_2606_15319_amd.layout import unpack_pages
+    T = k_pages.shape[2]
+    nf = (n_tokens + T - 1) // T
+    idx = torch.tensor(list(page_ids[:nf]), dtype=torch.long, device=k_pages.device)
+    kb = host_bits(k_pages.index_select(0, idx))
+    vb = host_bits(v_pages.index_select(0, idx))
+    k, v = unpack_pages(kb, vb, list(range(nf)), n_tokens)
+    return bits_to_f32(k), bits_to_f32(v)
 
 
 def frames_needed(shape, cache_len):
@@ -230,3 +276,82 @@ def sample_rows(L, seed=0, n_random=48):
     rows = set(range(0, min(L, 40))) | set(range(max(0, last - 8), L))
     rows |= set(int(r) for r in rng.choice(L, size=min(L, n_random), replace=False))
     return np.array(sorted(rows))
+
+
+# ------------------------------------------------------ stacks drawn on device
+class DeviceStack:
+    """An n_layers stack of one workload with every layer drawn on the device
+    by seeded torch generators, in the workload's distributions (matrices,
+    biases and mod_table N(0, 0.02^2), norm gains 1 + N(0, 0.02^2), cached
+    keys/values, text and x N(0, 1), bf16), and the streams' pages laid out as
+    the workload's (a wrapped ring when it has ring slots).  Layers the oracle
+    checks are copied back with host_layer."""
+
+    def __init__(self, wl, A, n_layers, seed, device="cuda"):
+        import torch
+        sh = wl.shape
+        self.wl, self.A, self.shape, self.n_layers = wl, A, sh, n_layers
+        D, H, d, T, L = sh.dim, sh.n_heads, sh.head_dim, sh.tokens_per_frame, sh.chunk_tokens
+        self.B = B = wl.n_streams
+        self.cache_len = [c * L for c in wl.cache_chunks]
+        self.frame_pos0 = list(wl.frame_pos0)
+        self.t = [float(wl.timesteps[i % len(wl.timesteps)]) for i in range(B)]
+        self.page_ids, self.n_pages = stream_page_ids(wl)
+        max_frames = max(len(p) for p in self.page_ids)
+        table = np.zeros((B, max_frames), np.int32)
+        for b, ids in enumerate(self.page_ids):
+            table[b, :len(ids)] = ids
+        self.table = dev_i32(table, device)
+        self.dims = A.dims_from_shape(sh)
+        self.batch = A.Batch([L] * B, self.cache_len, self.frame_pos0, [wl.ctx_len] * B)
+        self.ws_bytes = A.ardit_workspace_size(self.dims, self.batch)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        shapes = block_weight_shapes(sh)
+        self.w_dev, self.k, self.v, self.ctx, self.ctx_k, self.ctx_v = [], [], [], [], [], []
+        self.kv, self.w = [], []
+        for layer in range(n_layers):
+            g = torch.Generator(device=device)
+            g.manual_seed(seed + 1000 * layer)
+            wd = {}
+            for name, shp in shapes.items():
+                t = torch.randn(shp, generator=g, device=device) * 0.02
+                if name in GAIN_NAMES:
+                    t += 1.0
+                wd[name] = t if name == "mod_table" else t.to(torch.bfloat16)
+            kp = torch.randn((self.n_pages, H, T, d), generator=g, device=device).to(torch.bfloat16)
+            vp = torch.randn((self.n_pages, H, d, T), generator=g, device=device).to(torch.bfloat16)
+            ctx = torch.randn((B * wl.ctx_len, D), generator=g, device=device).to(torch.bfloat16)
+            ck = torch.empty(B * wl.ctx_len * D, dtype=torch.bfloat16, device=device)
+            cv = torch.empty_like(ck)
+            w = A.block_weights(wd)
+            A.ardit_ctx_kv(None, self.dims, self.batch, ctx, w, ck, cv, self.ws, self.ws_bytes)
+            self.w_dev.append(wd)
+            self.w.append(w)
+            self.k.append(kp)
+            self.v.append(vp)
+            self.ctx.append(ctx)
+            self.ctx_k.append(ck)
+            self.ctx_v.append(cv)
+            self.kv.append(A.kv_paged(kp, vp, self.table, self.n_pages, max_frames))
+        g = torch.Generator(device=device)
+        g.manual_seed(seed + 7)
+        tshapes = {"w_t1": (D, 256), "b_t1": (D,), "w_t2": (D, D), "b_t2": (D,),
+                   "w_m": (6 * D, D), "b_m": (6 * D,)}
+        self.tw_dev = {k: (torch.randn(s, generator=g, device=device) * 0.02).to(torch.bfloat16)
+                       for k, s in tshapes.items()}
+        self.x = torch.randn((B * L, D), generator=g, device=device).to(torch.bfloat16)
+        self.mod = torch.empty((B, 6, D), dtype=torch.float32, device=device)
+        A.ardit_time_mod(None, self.dims, self.t, A.time_weights(self.tw_dev), self.mod, self.ws,
+                         self.ws_bytes)
+
+    def host_layer(self, layer, b=0):
+        """(weights as fp32 numpy, cache keys [c, H, d], cache values, text [L_x, D])
+        of one layer and stream, copied back from the device."""
+        w = {k: host_f32(v) for k, v in self.w_dev[layer].items()}
+        ck, cv = read_stream_pages(self.k[layer], self.v[layer], self.page_ids[b], self.cache_len[b])
+        lx = self.wl.ctx_len
+        ctx = host_f32(self.ctx[layer])[b * lx:(b + 1) * lx]
+        return w, ck, cv, ctx
+
+    def time_weights_host(self):
+        return {k: host_f32(v) for k, v in self.tw_dev.items()}

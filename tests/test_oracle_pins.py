@@ -644,6 +644,35 @@ def test_fp8_weight_quantisation_within_bound():
         assert 1e-3 < rel < 0.1
 
 
+@pytest.mark.parametrize("n_keys", [14040, 32760])
+def test_fp8_statistical_criterion_discriminates(n_keys):
+    """The FP8 parity criterion (harness.fp8_parity) at the attention
+    workload's 14040 keys and the 1.3B-class block's 32760: the output of
+    attention whose softmax weights really are rounded to E4M3 per block of 32
+    keys (then stored bf16) passes, with errors of about one sigma in RMS (so
+    sigma is neither loose nor tight); an all-zero output, half the output and
+    a 2% scale error of the correctly quantised output all fail.  The
+    worst-case element bound is passed by the half output too, which is why
+    the criterion does not rest on it."""
+    from harness import fp8_parity
+    from workloads import bf16_round
+    rng = np.random.default_rng(90 + n_keys % 7)
+    H, d, R = 2, 128, 24
+    q = O.rms_norm(rng.standard_normal((R, H * d)), 1e-6).reshape(R, H, d)
+    k = O.rms_norm(rng.standard_normal((n_keys, H * d)), 1e-6).reshape(n_keys, H, d)
+    v = rng.standard_normal((n_keys, H, d))
+    o, bound, sig = F8.fp8_attention(q, k, v, sigma=True)
+    emul = bf16_round(F8.fp8_attention_quantized_weights(q, k, v))
+    msg = fp8_parity(emul, o, sig, "quantised weights")
+    z_rms = float(msg.split("z_rms=")[1].split()[0])
+    assert 0.6 <= z_rms <= 1.4, msg
+    for bad, tag in ((np.zeros_like(o), "zero"), (0.5 * o, "half"), (1.02 * emul, "2% scale")):
+        with pytest.raises(AssertionError):
+            fp8_parity(bad, o, sig, tag)
+    # the old element-wise worst case cannot tell half the output from the output
+    assert np.mean(np.abs(0.5 * o - o) <= bound) > 0.99
+
+
 # --------------------------------------------------------------------------
 # chunk generation: sampler, commit, sink + window
 # --------------------------------------------------------------------------
