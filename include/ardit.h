@@ -211,6 +211,28 @@ int ardit_kv_append(hipStream_t stream, const ardit_dims* dims, const ardit_batc
 int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
                    const void* q, const ardit_kv_paged* kv, void* o, void* ws, size_t ws_bytes);
 
+/* Paged attention without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops and harnesses
+ * that forbid hipMalloc).  Computes exactly what ardit_attn_fwd computes, with
+ * the same kernels and schedule, for batches whose streams all run bf16
+ * attention (dense or block-sparse); the scratch those kernels need (the
+ * split schedule's partial results, or the block selection's means, scores
+ * and lists) lives in a static device array of the library instead of the
+ * caller's workspace.  Limits: at most 72 MiB of scratch (the dense split
+ * schedule takes (2 * 256 * 256 * (head_dim + 2)) * 4 bytes: 65 MiB at
+ * head_dim 128; a sparse batch its ardit_sparse_select regions), else
+ * ARDIT_EWORKSPACE; a stream in FP8: ARDIT_EUNSUPPORTED; `stream` (NULL: the
+ * null stream of the current device) must belong to the current device, else
+ * ARDIT_EINVAL.  Each GPU holds one copy of the array, taken when the library
+ * is loaded and kept until the process ends, and every call on that GPU
+ * shares it: calls that overlap on one GPU (two streams, two threads) race on
+ * it and must be ordered by the caller.  Nothing needs clearing between calls
+ * (every scratch entry is written before it is read).  The call makes no
+ * device or host allocation, no memset and no copy; it records no timing
+ * events and skips ardit_debug_checks. */
+int ardit_attn_fwd_noalloc(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                           const void* q, const ardit_kv_paged* kv, void* o);
+
 /* The FP8 block quantisation the FP8 attention applies to its operands:
  * rows of bf16 x (device, row stride ld elements, ld % 8 == 0) to E4M3 codes
  * (device uint8 [rows][cols]) and E8M0 scales (device uint8 [rows][cols / 32]):

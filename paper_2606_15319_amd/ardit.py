@@ -105,6 +105,8 @@ _SIGS = {
                                   _P(ardit_kv_paged), _vp]),
     "ardit_attn_fwd": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
                                  _P(ardit_kv_paged), _vp, _vp, _sz]),
+    "ardit_attn_fwd_noalloc": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
+                                         _P(ardit_kv_paged), _vp]),
     "ardit_mx_quantize": (C.c_int, [_vp, _vp, C.c_int64, _i32, _i32, _vp, _vp]),
     "ardit_sparse_select": (C.c_int, [_vp, _P(ardit_dims), _P(ardit_batch), _vp,
                                       _P(ardit_kv_paged), _vp, _i32, _vp, _sz]),
@@ -268,6 +270,11 @@ def ardit_kv_append(stream, dims, batch: Batch, qkv, g_q, g_k, kv: ardit_kv_page
 def ardit_attn_fwd(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o, ws, ws_bytes):
     _check(_lib.ardit_attn_fwd(_stream(stream), C.byref(dims), C.byref(batch.struct), _ptr(q),
                                C.byref(kv), _ptr(o), _ptr(ws), int(ws_bytes)), "ardit_attn_fwd")
+
+
+def ardit_attn_fwd_noalloc(stream, dims, batch: Batch, q, kv: ardit_kv_paged, o):
+    _check(_lib.ardit_attn_fwd_noalloc(_stream(stream), C.byref(dims), C.byref(batch.struct),
+                                       _ptr(q), C.byref(kv), _ptr(o)), "ardit_attn_fwd_noalloc")
 
 
 QUANT_BF16, QUANT_FP8 = 0, 1

@@ -782,6 +782,44 @@ int check_block_args(hipStream_t st, const ardit_dims* d, const ardit_batch* b, 
   return check_pages(st, d, b, kv, true);
 }
 
+// ------------------------------------------------ allocation-free attention
+// Scratch of ardit_attn_fwd_noalloc: the split schedule's partial results
+// (dense batches) or the block selection's means, scores and lists (sparse
+// batches).  One copy per GPU the library runs on, held until the process
+// ends.  Host code never uses the array's name as an address: the device
+// address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = static_cast<size_t>(72) << 20;
+constexpr int kScratchDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on device dev, which must be current.
+int scratch_address(int dev, void** out) {
+  static std::mutex mu;
+  static void* addr[kScratchDevices] = {};
+  if (dev < 0 || dev >= kScratchDevices)
+    return fail(ARDIT_EUNSUPPORTED, "device %d beyond the %d the scratch table covers", dev,
+                kScratchDevices);
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    ARDIT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(ARDIT_EHIP, "hipGetSymbolAddress(scratch) gave a null address");
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return ARDIT_OK;
+}
+
+// Scratch bytes a batch's self-attention needs: the sparse selection's
+// regions, else the split schedule's partial results.
+size_t noalloc_scratch_bytes(const ardit_dims* d, const ardit_batch* b) {
+  if (batch_sparse(b)) {
+    const SparseBytes sp = sparse_ws_bytes(d, b);
+    return up(sp.qbar) + up(sp.scores) + up(sp.lists);
+  }
+  return up(attention_split_bytes(d->head_dim));
+}
+
 }  // namespace
 
 namespace ardit {
@@ -925,6 +963,50 @@ int ardit_attn_fwd(hipStream_t stream, const ardit_dims* dims, const ardit_batch
   ARDIT_TRY(check_ws(dims, batch, ws, ws_bytes, &L));
   ARDIT_TRY(check_pages(stream, dims, batch, kv, false));
   return self_attention(stream, dims, batch, q, kv, o, ws, L);
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_attn_fwd_noalloc(hipStream_t stream, const ardit_dims* dims, const ardit_batch* batch,
+                           const void* q, const ardit_kv_paged* kv, void* o) try {
+  ARDIT_TRY(check_dims(dims));
+  ARDIT_TRY(check_batch(dims, batch, kUseQ | kUseCache));
+  ARDIT_TRY(check_kv(dims, batch, kv));
+  ARDIT_TRY(check_sparse(dims, batch));
+  ARDIT_TRY(check_ptr(q, "q"));
+  ARDIT_TRY(check_ptr(o, "o"));
+  if (batch_fp8(batch))
+    return fail(ARDIT_EUNSUPPORTED, "the allocation-free attention runs bf16 streams only");
+  const size_t need = noalloc_scratch_bytes(dims, batch);
+  if (need > kScratchBytes)
+    return fail(ARDIT_EWORKSPACE, "batch needs %zu bytes of scratch, above the %zu the "
+                "allocation-free attention holds", need, kScratchBytes);
+  int dev = -1;
+  ARDIT_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (stream) {
+    hipDevice_t sdev = -1;
+    ARDIT_HIP(hipStreamGetDevice(stream, &sdev), "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(ARDIT_EINVAL, "the stream belongs to device %d, device %d is current", sdev,
+                  dev);
+  }
+  void* base = nullptr;
+  ARDIT_TRY(scratch_address(dev, &base));
+  AttnArgs a = self_attn_base(dims, batch, q, kv, o);
+  const int hd = dims->head_dim;
+  if (batch_sparse(batch)) {
+    const SparseBytes sp = sparse_ws_bytes(dims, batch);
+    char* c = static_cast<char*>(base);
+    plan_sparse_attention(a, batch->sparsity, reinterpret_cast<int32_t*>(c + up(sp.qbar) +
+                                                                           up(sp.scores)),
+                          0, reinterpret_cast<float*>(c), reinterpret_cast<float*>(c + up(sp.qbar)));
+    ARDIT_HIP(launch_sparse_select(stream, a, hd), "block selection launch");
+    ARDIT_HIP(launch_sparse_attention(stream, a, hd), "block-sparse attention launch");
+  } else {
+    plan_attention(a, hd, static_cast<float*>(base));
+    ARDIT_HIP(launch_attention(stream, a, hd, true), "self-attention launch");
+  }
+  return ARDIT_OK;
 } catch (...) {
   return host_failure();
 }

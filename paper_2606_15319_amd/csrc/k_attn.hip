@@ -29,8 +29,7 @@
 // results (unnormalised O, running max and denominator in fp32) that a second
 // kernel merges.
 #include <math.h>
-
-#include <vector>
+#include <string.h>
 
 #include "launch.h"
 
@@ -850,34 +849,58 @@ namespace {
 
 constexpr int kCusPerXcd = 32;   // MI355X: 8 XCDs of 32 CUs
 
-// List schedule of item costs [i, n) (plan order) onto one XCD's CUs, each CU
+// Item costs in plan order as runs: the items of one stream are contiguous
+// and cost the same (its key tiles, or its kept tiles when sparse), so run r
+// covers items [begin[r], begin[r + 1]) at cost[r].
+struct CostRuns {
+  int n;
+  int32_t begin[kMaxStreams + 1];
+  int32_t cost[kMaxStreams];
+};
+
+// List schedule of items [i, n) (plan order) onto one XCD's CUs, each CU
 // taking the next item when it frees (how the dispatcher hands out an XCD's
 // workgroups in order, one 512-thread workgroup per CU).  Returns the first
 // item past those that finish by makespan M; with share > 0 it also stops once
 // the XCD's cost reaches share.
-int fill_xcd(const int32_t* cost, int i, int n, int64_t M, int64_t share) {
+int fill_xcd(const CostRuns& c, int i, int n, int64_t M, int64_t share) {
   int64_t fin[kCusPerXcd] = {};
   int64_t taken = 0;
+  int r = 0;
+  while (r + 1 < c.n && i >= c.begin[r + 1]) ++r;
   for (; i < n; ++i) {
+    while (i >= c.begin[r + 1]) ++r;
+    const int64_t cost = c.cost[r];
     if (share > 0 && taken >= share) break;
     int k = 0;
-    for (int c = 1; c < kCusPerXcd; ++c) k = fin[c] < fin[k] ? c : k;
-    if (fin[k] + cost[i] > M) break;
-    fin[k] += cost[i];
-    taken += cost[i];
+    for (int u = 1; u < kCusPerXcd; ++u) k = fin[u] < fin[k] ? u : k;
+    if (fin[k] + cost > M) break;
+    fin[k] += cost;
+    taken += cost;
   }
   return i;
+}
+
+int64_t runs_cost(const CostRuns& c, int i0, int i1) {
+  int64_t t = 0;
+  for (int r = 0; r < c.n; ++r) {
+    const int lo = c.begin[r] > i0 ? c.begin[r] : i0;
+    const int hi = c.begin[r + 1] < i1 ? c.begin[r + 1] : i1;
+    if (hi > lo) t += static_cast<int64_t>(hi - lo) * c.cost[r];
+  }
+  return t;
 }
 
 // Contiguous split of the items over the XCDs that minimises the makespan of
 // the slowest XCD under list scheduling (binary search on the makespan), with
 // the items spread evenly by cost where that makespan allows.
-void split_by_makespan(const int32_t* cost, int n, int64_t total, int32_t* begin) {
+void split_by_makespan(const CostRuns& c, int n, int64_t total, int32_t* begin) {
   int64_t lo = 0, hi = total;
-  for (int i = 0; i < n; ++i) lo = cost[i] > lo ? cost[i] : lo;
+  for (int r = 0; r < c.n; ++r)
+    if (c.begin[r + 1] > c.begin[r]) lo = c.cost[r] > lo ? c.cost[r] : lo;
   auto feasible = [&](int64_t M) {
     int i = 0;
-    for (int x = 0; x < kNumXcd && i < n; ++x) i = fill_xcd(cost, i, n, M, 0);
+    for (int x = 0; x < kNumXcd && i < n; ++x) i = fill_xcd(c, i, n, M, 0);
     return i == n;
   };
   while (lo < hi) {
@@ -896,8 +919,8 @@ void split_by_makespan(const int32_t* cost, int n, int64_t total, int32_t* begin
         share = (total - done) / (kNumXcd - x);
         share = share > 0 ? share : 1;
       }
-      const int e = fill_xcd(cost, i, n, lo, share);
-      for (int j = i; j < e; ++j) done += cost[j];
+      const int e = fill_xcd(c, i, n, lo, share);
+      done += runs_cost(c, i, e);
       i = e;
       begin[x + 1] = i;
     }
@@ -906,40 +929,46 @@ void split_by_makespan(const int32_t* cost, int n, int64_t total, int32_t* begin
 }
 
 // The last plan's XCD split, reused while the item costs repeat (every layer
-// and denoising step of a chunk has the same geometry).
+// and denoising step of a chunk has the same geometry).  Fixed-size, so
+// planning makes no host allocation.
 struct XcdSplitCache {
-  std::vector<int32_t> key;
+  int32_t key[2 * kMaxStreams + 1];
+  int key_len = -1;
   int32_t begin[kNumXcd + 1];
 };
 
 }  // namespace
 
 void balance_items_over_xcds(AttnArgs& a, bool sparse) {
-  // per-item cost in plan order, compressed per stream for the cache key
+  // per-stream item runs in plan order, also the cache key
   thread_local XcdSplitCache cache;
-  std::vector<int32_t> key;
-  key.reserve(2 * a.n_streams + 1);
-  key.push_back(a.H);
+  int32_t key[2 * kMaxStreams + 1];
+  int key_len = 0;
+  key[key_len++] = a.H;
+  CostRuns runs;
+  runs.n = a.n_streams;
   int64_t total = 0;
   for (int i = 0; i < a.n_streams; ++i) {
     const int32_t c = sparse ? a.s[i].n_keep : a.s[i].n_tiles;
-    key.push_back(a.s[i].n_qtiles);
-    key.push_back(c);
+    key[key_len++] = a.s[i].n_qtiles;
+    key[key_len++] = c;
+    runs.begin[i] = a.s[i].item_begin;
+    runs.cost[i] = c;
     total += static_cast<int64_t>(a.s[i].n_qtiles) * a.H * c;
   }
   const int n = a.total_items;
-  if (key != cache.key) {
+  runs.begin[a.n_streams] = n;
+  const bool same = key_len == cache.key_len &&
+                    memcmp(key, cache.key, sizeof(int32_t) * static_cast<size_t>(key_len)) == 0;
+  if (!same) {
     if (n <= 65536) {
-      std::vector<int32_t> cost(n);
-      for (int i = 0; i < a.n_streams; ++i)
-        for (int j = 0; j < a.s[i].n_qtiles * a.H; ++j)
-          cost[a.s[i].item_begin + j] = sparse ? a.s[i].n_keep : a.s[i].n_tiles;
-      split_by_makespan(cost.data(), n, total, cache.begin);
+      split_by_makespan(runs, n, total, cache.begin);
     } else {   // very large batches: equal item counts
       for (int x = 0; x <= kNumXcd; ++x)
         cache.begin[x] = static_cast<int32_t>(static_cast<int64_t>(n) * x / kNumXcd);
     }
-    cache.key = key;
+    memcpy(cache.key, key, sizeof(int32_t) * static_cast<size_t>(key_len));
+    cache.key_len = key_len;
   }
   int most = 0;
   for (int x = 0; x <= kNumXcd; ++x) a.xcd_begin[x] = cache.begin[x];

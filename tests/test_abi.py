@@ -341,3 +341,18 @@ def test_debug_checks_switch():
     assert _status(A.ardit_debug_checks, -1) == -1
     A.ardit_debug_checks(1)
     A.ardit_debug_checks(0)
+
+
+def test_noalloc_attention_host_rejections():
+    """The allocation-free attention refuses, before touching the device, FP8
+    streams and batches whose scratch exceeds its 72 MiB."""
+    d = _dims(dim=512, n_heads=4, head_dim=128)
+    assert _status(A.ardit_attn_fwd_noalloc, FAKE, d, A.Batch([64], [256], quant=[1]), FAKE,
+                   _kv(max_frames=9), FAKE) == -5
+    # 2048 items x 10048 key tiles of fp32 scores alone are 82 MB
+    big = A.Batch([131072], [512000], sparsity=[0.9])
+    assert _status(A.ardit_attn_fwd_noalloc, FAKE, d, big, FAKE, _kv(max_frames=10048),
+                   FAKE) == -4
+    assert "72" in A.ardit_last_error() or "scratch" in A.ardit_last_error()
+    assert _status(A.ardit_attn_fwd_noalloc, FAKE, d, A.Batch([64], [256]), 0,
+                   _kv(max_frames=9), FAKE) == -1
