@@ -167,8 +167,7 @@ __device__ __forceinline__ void store_output(const AttnArgs& a, const AttnStream
   const int l16 = lane & 15, g = lane >> 4;
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float l_tot = rows4_sum(l_run[qb]);
     const float inv = 1.0f / l_tot;
     const int ql = qt * BQ + wave * 32 + 16 * qb + l16;
     if (ql < S.q_len) {
@@ -194,8 +193,7 @@ __device__ __forceinline__ void store_partial(const AttnArgs& a, size_t slot,
   const int l16 = lane & 15, g = lane >> 4;
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float l_tot = rows4_sum(l_run[qb]);
     const int row = wave * 32 + 16 * qb + l16;
     float* po = a.part_o + (slot * BQ + row) * HD;
 #pragma unroll
@@ -382,8 +380,7 @@ __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& 
           for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kb][qb][v]);
-          mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-          mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+          mx = rows4_max(mx) * c;
           if (__any(mx > m_run[qb] + 8.0f)) {
             const float m_new = fmaxf(m_run[qb], mx);
             const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
@@ -397,18 +394,20 @@ __device__ __forceinline__ void attn_range(const AttnArgs& a, const AttnStream& 
           const float mr = m_run[qb];
 #pragma unroll
           for (int ps = 0; ps < 2; ++ps) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float pv =
-                  __builtin_amdgcn_exp2f(fmaf(s[2 * ps + (e >> 2)][qb][e & 3], c, -mr));
-              pf[qb][ps][e] = static_cast<__bf16>(pv);
-            }
+            uint32_t pw[4];
             const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-              const bf16x2 pp = {pf[qb][ps][e], pf[qb][ps][e + 1]};
-              l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run[qb], false);
+            for (int e2 = 0; e2 < 4; ++e2) {
+              const int e = 2 * e2;
+              const float p0 =
+                  __builtin_amdgcn_exp2f(fmaf(s[2 * ps + (e >> 2)][qb][e & 3], c, -mr));
+              const float p1 = __builtin_amdgcn_exp2f(
+                  fmaf(s[2 * ps + ((e + 1) >> 2)][qb][(e + 1) & 3], c, -mr));
+              pw[e2] = pack_bf16x2(p0, p1);
+              l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[e2]),
+                                                          one2, l_run[qb], false);
             }
+            pf[qb][ps] = __builtin_bit_cast(bf16x8, u32x4{pw[0], pw[1], pw[2], pw[3]});
           }
         }
         // O^T += V^T P^T: 16-dim blocks x two query blocks, 16 accumulators
@@ -630,8 +629,7 @@ __global__ __launch_bounds__(NTHR, 1) void attn_kernel(const AttnArgs a) {
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int v = 0; v < 4; ++v) mx = fmaxf(mx, s[kb][qb][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+      mx = rows4_max(mx) * c;
       if (__any(mx > m_run[qb] + 8.0f)) {
         const float m_new = fmaxf(m_run[qb], mx);
         const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
@@ -645,17 +643,23 @@ __global__ __launch_bounds__(NTHR, 1) void attn_kernel(const AttnArgs a) {
       const float mr = m_run[qb];
 #pragma unroll
       for (int ps = 0; ps < 2; ++ps) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = __builtin_amdgcn_exp2f(fmaf(s[2 * ps + (e >> 2)][qb][e & 3], c, -mr));
-          pf[qb][ps][e] = static_cast<__bf16>(pv);
-        }
+        // keys 2 e2, 2 e2 + 1 of the step packed into one register, which both
+        // feeds the P operand and is summed into the denominator (a plain
+        // array: filling a 4-word vector element by element here compiled to
+        // dot products that all read its first word)
+        uint32_t pw[4];
         const bf16x2 one2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const bf16x2 pp = {pf[qb][ps][e], pf[qb][ps][e + 1]};
-          l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pp, one2, l_run[qb], false);
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const int e = 2 * e2;
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * ps + (e >> 2)][qb][e & 3], c, -mr));
+          const float p1 =
+              __builtin_amdgcn_exp2f(fmaf(s[2 * ps + ((e + 1) >> 2)][qb][(e + 1) & 3], c, -mr));
+          pw[e2] = pack_bf16x2(p0, p1);
+          l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[e2]), one2,
+                                                      l_run[qb], false);
         }
+        pf[qb][ps] = __builtin_bit_cast(bf16x8, u32x4{pw[0], pw[1], pw[2], pw[3]});
       }
     }
     // O^T += V^T P^T: 16-dim blocks x two query blocks, 16 accumulators
@@ -691,8 +695,7 @@ __global__ __launch_bounds__(NTHR, 1) void attn_kernel(const AttnArgs a) {
 
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float l_tot = rows4_sum(l_run[qb]);
     const float inv = 1.0f / l_tot;
     if (q_local[qb] < S.q_len) {
       bf16_t* op = a.o + static_cast<size_t>(S.q_off + q_local[qb]) * a.ldo + h * HD;
