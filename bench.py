@@ -41,9 +41,15 @@ step is one ardit_chunk_generate of the same chunk (4 denoising steps at
 at t = 0), the cache being chunks 0..5 of a window of W = 7 chunks (no sink)
 while chunk 6 is generated; value = ms per chunk.
 
---append-probe only times ardit_kv_append (the elementwise key and value
-append) on 8 x 4680 rows, warm and with the caches flushed before each call,
-and prints one line with both rates."""
+--micro only runs the measurement kernels (include/ardit_micro.h): MFMA
+throughput in bf16 and fp8 with register operands, and a 1 GiB device copy;
+the default run also measures them (a few ms) and reports each roofline
+against the measured peak besides the published one.
+
+--workload ragged --cold times every elementwise launch of one step of the
+8-stream batch twice: after a 512 MiB buffer is read (neither L2 nor the
+256 MB last-level cache holds the operands, and neither holds dirty lines) and
+back to back, per kernel."""
 from __future__ import annotations
 
 import argparse
@@ -86,9 +92,12 @@ def parse():
                    help="time whole-chunk generation (4 steps + commit) of the 1.3B-class stack")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB on the device 5 times with one kernel (counter calibration)")
-    p.add_argument("--append-probe", action="store_true",
-                   help="only time ardit_kv_append on 8 x 4680 rows of the 1.3B-class block, "
-                        "back to back and with the caches flushed before every call")
+    p.add_argument("--micro", action="store_true",
+                   help="only run the measurement kernels: MFMA throughput (bf16, fp8) and "
+                        "the HBM copy, and print one line with the measured peaks")
+    p.add_argument("--cold", action="store_true",
+                   help="with --workload ragged: time every elementwise launch of one step "
+                        "after a 512 MiB write (cold caches) and warm, per kernel")
     return p.parse_args()
 
 
@@ -138,57 +147,103 @@ def copy_probe(mib):
     log(f"copied {mib} MiB 5 times ({mib * (1 << 20)} bytes read and written per copy)")
 
 
-def append_probe():
-    """ardit_kv_append (QK-norm + RoPE + key append and value append, 12ND bytes)
-    over 8 streams of 4680 rows: warm (back to back) and cold (a 512 MiB buffer
-    written before each call, so neither L2 nor the 256 MB last-level cache
-    holds the operands)."""
+def measured_peaks(A, reps=3):
+    """Measured MFMA throughput (bf16, fp8; TFLOP/s) and HBM copy bandwidth
+    (TB/s, bytes read + written) with the library's measurement kernels, best
+    of `reps` launches each."""
     import torch
-    from paper_2606_15319_amd import ardit as A
-    from workloads import WORKLOADS
-    sh = WORKLOADS["block13b"].shape
-    B, L, D, H, d, T = 8, sh.chunk_tokens, sh.dim, sh.n_heads, sh.head_dim, sh.tokens_per_frame
-    N = B * L
-    dev = torch.device("cuda:0")
-    g = torch.Generator(device=dev)
-    g.manual_seed(15319)
-    qkv = torch.randn((N, 3 * D), generator=g, device=dev).to(torch.bfloat16)
-    g_q = (1 + 0.02 * torch.randn((D,), generator=g, device=dev)).to(torch.bfloat16)
-    g_k = (1 + 0.02 * torch.randn((D,), generator=g, device=dev)).to(torch.bfloat16)
-    n_pages = B * sh.frames
-    kp = torch.empty((n_pages, H, T, d), dtype=torch.bfloat16, device=dev)
-    vp = torch.empty((n_pages, H, d, T), dtype=torch.bfloat16, device=dev)
-    table = torch.arange(n_pages, dtype=torch.int32, device=dev).reshape(B, sh.frames)
-    kv = A.kv_paged(kp, vp, table, n_pages, sh.frames)
-    dims = A.dims_from_shape(sh)
-    batch = A.Batch([L] * B, [0] * B, [0] * B)
-    q_out = torch.empty((N, D), dtype=torch.bfloat16, device=dev)
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    call = lambda: A.ardit_kv_append(None, dims, batch, qkv, g_q, g_k, kv, q_out)  # noqa: E731
-    nbytes = 12 * N * D
-    call()
-    torch.cuda.synchronize()
-    reps = 20
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        call()
-    e1.record()
-    torch.cuda.synchronize()
-    warm_ms = e0.elapsed_time(e1) / reps
-    cold = []
-    for _ in range(reps):
-        flush.fill_(1)
+    wgs = 256 * 2 * 4        # 2 workgroups of 4 waves per CU, four rounds
+    sink = torch.empty(wgs * 256, dtype=torch.float32, device="cuda")
+    out = {}
+    for name, dtype, iters in (("mfma_bf16", 0, 2000), ("mfma_fp8", 1, 2000)):
+        best = 0.0
+        for r in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            flops = A.ardit_micro_mfma(None, dtype, wgs, iters, sink)
+            e1.record()
+            torch.cuda.synchronize()
+            if r:
+                best = max(best, flops / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+        out[name + "_tflops"] = round(best, 1)
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    A.ardit_micro_fill(None, src, nbytes, 0x3f800000)
+    best = 0.0
+    for r in range(reps + 2):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        call()
+        A.ardit_micro_copy(None, src, dst, nbytes)
         e1.record()
         torch.cuda.synchronize()
-        cold.append(e0.elapsed_time(e1))
-    cold_ms = sorted(cold)[reps // 2]
-    print(json.dumps({"probe": "ardit_kv_append", "rows": N, "bytes": nbytes,
-                      "warm_ms": round(warm_ms, 4), "warm_TBps": round(nbytes / warm_ms / 1e9, 3),
-                      "cold_ms_median": round(cold_ms, 4),
-                      "cold_TBps": round(nbytes / cold_ms / 1e9, 3)}), flush=True)
+        if r:
+            best = max(best, 2 * nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    out["copy_tbps"] = round(best, 3)
+    sink = torch.empty(32 << 10, dtype=torch.uint8, device="cuda")
+    best = 0.0
+    for r in range(reps + 2):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        A.ardit_micro_read(None, src, nbytes, sink, sink.numel())
+        e1.record()
+        torch.cuda.synchronize()
+        if r:
+            best = max(best, nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    out["read_tbps"] = round(best, 3)
+    del src, dst
+    torch.cuda.synchronize()
+    return out
+
+
+def micro_main():
+    import torch
+    from paper_2606_15319_amd import ardit as A
+    torch.cuda.set_device(0)
+    m = measured_peaks(A, reps=5)
+    m.update({"probe": "measurement kernels",
+              "note": "MFMA: 2048 workgroups x 4 waves, 2000 iterations of independent register "
+                      "chains (bf16 8 x v_mfma_f32_16x16x32_bf16, fp8 4 x "
+                      "v_mfma_scale_f32_32x32x64_f8f6f4); copy: 1 GiB read + 1 GiB written, "
+                      "read: 1 GiB read, 16-byte accesses four in flight per thread; best of 5",
+              "published": {"mfma_bf16_tflops": PEAK_BF16_TFLOPS, "mfma_fp8_tflops": PEAK_FP8_TFLOPS,
+                            "hbm_tbps": 8.0}})
+    print(json.dumps(m), flush=True)
+
+
+# bytes each elementwise launch of a block moves per token row and hidden
+# unit: inputs read once, outputs written once (bf16 2 bytes, fp32 4)
+ELEMENTWISE_BYTES_PER_ND = {"adaln_norm": 4, "qk_norm_rope / kv append": 12, "cross pre-norm": 6,
+                            "cross q-norm": 4, "adaln_norm 2": 6}
+
+
+def cold_elementwise(A, model, sh, n_rows):
+    """Every elementwise launch of one step, cold (a 512 MiB read before each)
+    and warm (back to back), grouped by kernel: median ms and TB/s."""
+    import statistics
+    import torch
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    res = {}
+    for mode in ("cold", "warm"):
+        A.ardit_timing_flush(flush if mode == "cold" else None, flush.numel() if mode == "cold" else 0)
+        A.ardit_timing_enable(1 << A.TIME_ELEMENTWISE)
+        model.step(0)
+        torch.cuda.synchronize()
+        A.ardit_timing_enable(False)
+        A.ardit_timing_flush(None, 0)
+        recs = A.ardit_timing_records(A.TIME_ELEMENTWISE)
+        by = {}
+        for name, ms in recs:
+            by.setdefault(name, []).append(ms)
+        for name, v in by.items():
+            ms = statistics.median(v)
+            nbytes = ELEMENTWISE_BYTES_PER_ND[name] * n_rows * sh.dim
+            res.setdefault(name, {"bytes": nbytes, "launches": len(v)})
+            res[name][mode + "_ms"] = round(ms, 4)
+            res[name][mode + "_TBps"] = round(nbytes / (ms * 1e-3) / 1e12, 3)
+    for r in res.values():
+        r["cold_frac_of_8TBps"] = round(r["cold_TBps"] / 8.0, 3)
+    return res
 
 
 class Model:
@@ -427,9 +482,12 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
-    if args.append_probe:
-        append_probe()
+    if args.micro:
+        micro_main()
         return
+    if args.cold and args.workload != "ragged":
+        print("--cold times the elementwise kernels of the ragged workload only", file=sys.stderr)
+        sys.exit(2)
     if args.chunk and args.workload == "large":
         args.workload = "block13b"
     if args.chunk and (args.workload != "block13b" or args.sparsity or args.quant != "bf16"):
@@ -451,6 +509,15 @@ def main():
     model = Model(A, wl, args.layers, dev, rho=args.sparsity,
                   timesteps=[float(t) for t in wl.timesteps] if ragged else None,
                   fp8=args.quant == "fp8")
+    if args.cold:
+        model.step(0)
+        torch.cuda.synchronize()
+        res = cold_elementwise(A, model, sh, sh.chunk_tokens * len(cache_lens))
+        print(json.dumps({"probe": "elementwise kernels, cold and warm",
+                          "workload": workload_name(wl, args), "rows": sh.chunk_tokens * len(cache_lens),
+                          "flush": "512 MiB read before each cold launch",
+                          "kernels": res}), flush=True)
+        return
     if args.chunk:
         model.setup_chunk(TIMESTEPS, window=7)
         run = lambda k: model.generate()   # noqa: E731
@@ -507,6 +574,14 @@ def main():
                               "(extrapolated)")
         log(f"oracle: {cpu['value']} ms on {cpu['cores']} threads")
     peak = PEAK_FP8_TFLOPS if args.quant == "fp8" else PEAK_BF16_TFLOPS
+    log("measuring the MFMA and copy peaks")
+    meas = measured_peaks(A)
+    meas_peak = meas["mfma_fp8_tflops" if args.quant == "fp8" else "mfma_bf16_tflops"]
+    if breakdown:
+        breakdown["gemm"]["frac_of_measured"] = round(
+            breakdown["gemm"]["achieved"] / meas["mfma_bf16_tflops"], 4)
+        breakdown["elementwise"]["frac_of_measured"] = round(
+            breakdown["elementwise"]["achieved"] / meas["copy_tbps"], 4)
     line = {
         "metric": "ms per chunk" if args.chunk else "ms per chunk-denoise-step per block",
         "value": round(ms_step if args.chunk else ms_block, 4),
@@ -535,7 +610,10 @@ def main():
                      "kernel": (("FP8 " if args.quant == "fp8" else "")
                                 + ("block-sparse " if args.sparsity else "")
                                 + "paged self-attention"),
-                     "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn},
+                     "avg_launch_ms": round(attn_avg_ms, 4), "launches": n_attn,
+                     "measured_peak": meas_peak,
+                     "frac_of_measured": round(achieved / meas_peak, 4) if meas_peak else None},
+        "measured_peaks": meas,
         "breakdown": breakdown,
         "cpu_baseline": cpu,
     }

@@ -372,6 +372,22 @@ int ardit_timing_enable(int enable);
 int ardit_timing_collect(int32_t* launches, double* total_ms);
 int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms);
 
+/* Cold timing and per-launch records.  ardit_timing_flush(buf, bytes) makes
+ * every timed launch (the kinds enabled by ardit_timing_enable) first read
+ * device buffer buf (16-byte aligned, bytes % 16 == 0, at least 128 KiB; its
+ * last 64 KiB receive the read's checksum words) with a kernel outside its
+ * events, so a buffer larger than L2 and the last-level cache leaves the
+ * launch's operands cold and the caches holding clean lines (a write would
+ * leave dirty lines to be written back during the timed launch); (NULL, 0)
+ * turns it off.
+ * ardit_timing_records waits for the recorded launches of one kind and
+ * returns, in launch order, each launch's name (a static string of the
+ * library) and duration in ms, clearing them; ARDIT_ECAPACITY (nothing
+ * cleared, *n_records set to the count) when more than max_records are held. */
+int ardit_timing_flush(void* buf, size_t bytes);
+int ardit_timing_records(int32_t kind, int32_t max_records, const char** names, double* ms,
+                         int32_t* n_records);
+
 /* Debug validation of page tables (off by default; for callers that want a
  * bad table reported rather than silently dropped or clamped).  With
  * ardit_debug_checks(1) every call that reads a page table first copies it to

@@ -134,6 +134,12 @@ _SIGS = {
     "ardit_timing_collect": (C.c_int, [_P(_i32), _P(C.c_double)]),
     "ardit_timing_collect_kind": (C.c_int, [_i32, _P(_i32), _P(C.c_double)]),
     "ardit_debug_checks": (C.c_int, [C.c_int]),
+    "ardit_timing_flush": (C.c_int, [_vp, _sz]),
+    "ardit_timing_records": (C.c_int, [_i32, _i32, _P(C.c_char_p), _P(C.c_double), _P(_i32)]),
+    "ardit_micro_mfma": (C.c_int, [_vp, _i32, _i32, _i32, _vp, _P(C.c_double)]),
+    "ardit_micro_copy": (C.c_int, [_vp, _vp, _vp, _sz]),
+    "ardit_micro_read": (C.c_int, [_vp, _vp, _sz, _vp, _sz]),
+    "ardit_micro_fill": (C.c_int, [_vp, _vp, _sz, C.c_uint32]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -369,6 +375,44 @@ def ardit_timing_collect_kind(kind):
     _check(_lib.ardit_timing_collect_kind(int(kind), C.byref(n), C.byref(ms)),
            "ardit_timing_collect_kind")
     return n.value, ms.value
+
+
+def ardit_timing_flush(buf, nbytes):
+    """buf: device buffer written before every timed launch (None, 0: off)."""
+    _check(_lib.ardit_timing_flush(_ptr(buf), int(nbytes)), "ardit_timing_flush")
+
+
+def ardit_timing_records(kind, max_records=4096):
+    """[(launch name, ms)] of the timed launches of one kind, in launch order."""
+    names = (C.c_char_p * max(max_records, 1))()
+    ms = (C.c_double * max(max_records, 1))()
+    n = C.c_int32(0)
+    _check(_lib.ardit_timing_records(int(kind), int(max_records), names, ms, C.byref(n)),
+           "ardit_timing_records")
+    return [(names[i].decode(), ms[i]) for i in range(n.value)]
+
+
+def ardit_micro_mfma(stream, dtype, workgroups, iters, sink):
+    """Launches the MFMA throughput kernel; returns the flops it performs."""
+    f = C.c_double(0.0)
+    _check(_lib.ardit_micro_mfma(_stream(stream), int(dtype), int(workgroups), int(iters),
+                                 _ptr(sink), C.byref(f)), "ardit_micro_mfma")
+    return f.value
+
+
+def ardit_micro_copy(stream, src, dst, nbytes):
+    _check(_lib.ardit_micro_copy(_stream(stream), _ptr(src), _ptr(dst), int(nbytes)),
+           "ardit_micro_copy")
+
+
+def ardit_micro_read(stream, src, nbytes, sink, sink_bytes):
+    _check(_lib.ardit_micro_read(_stream(stream), _ptr(src), int(nbytes), _ptr(sink),
+                                 int(sink_bytes)), "ardit_micro_read")
+
+
+def ardit_micro_fill(stream, dst, nbytes, value=0):
+    _check(_lib.ardit_micro_fill(_stream(stream), _ptr(dst), int(nbytes), int(value)),
+           "ardit_micro_fill")
 
 
 def ardit_debug_checks(enable):

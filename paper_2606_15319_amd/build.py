@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libardit.so")
 SOURCES = ["api.cpp", "k_gemm.hip", "k_attn.hip", "k_elem.hip", "k_sparse.hip", "k_fp8.hip",
-           "k_chunk.hip", "control.cpp"]
+           "k_chunk.hip", "k_micro.hip", "control.cpp"]
 
 
 def hipcc() -> str:

@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "ardit.h"
+#include "ardit_micro.h"
 #include "launch.h"
 
 using namespace ardit;
@@ -419,12 +420,16 @@ enum TimedKind : int { kTimeAttn = 0, kTimeGemm = 1, kTimeElem = 2, kTimeKinds =
 
 struct TimedRec {
   int kind;
+  const char* what;   // static string naming the launch
   hipEvent_t e0, e1;
 };
 
 struct Timing {
   std::mutex mu;
   unsigned mask = 0;
+  void* flush = nullptr;     // read before every timed launch when set (cold caches)
+  size_t flush_bytes = 0;
+  uint32_t* flush_sink = nullptr;   // one word per workgroup of the flush read
   std::vector<hipEvent_t> pool;
   std::vector<TimedRec> rec;
 };
@@ -449,22 +454,36 @@ hipEvent_t take_event(Timing& t) {
 struct TimedLaunch {
   hipStream_t st;
   int kind;
+  const char* what;
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  TimedLaunch(hipStream_t s, int k) : st(s), kind(k) {
+  void* flush = nullptr;
+  size_t flush_bytes = 0;
+  uint32_t* flush_sink = nullptr;
+  TimedLaunch(hipStream_t s, int k, const char* w) : st(s), kind(k), what(w) {
     Timing& tm = timing();
     std::lock_guard<std::mutex> g(tm.mu);
     if (tm.mask & (1u << k)) {
       e0 = take_event(tm);
       e1 = take_event(tm);
+      flush = tm.flush;
+      flush_bytes = tm.flush_bytes;
+      flush_sink = tm.flush_sink;
     }
   }
-  hipError_t begin() { return e0 && e1 ? hipEventRecord(e0, st) : hipSuccess; }
+  hipError_t begin() {
+    if (!(e0 && e1)) return hipSuccess;
+    if (flush) {
+      const hipError_t f = launch_micro_read(st, flush, flush_bytes, flush_sink);
+      if (f != hipSuccess) return f;
+    }
+    return hipEventRecord(e0, st);
+  }
   hipError_t end() {
     if (!(e0 && e1)) return hipSuccess;
     const hipError_t e = hipEventRecord(e1, st);
     Timing& tm = timing();
     std::lock_guard<std::mutex> g(tm.mu);
-    tm.rec.push_back(TimedRec{kind, e0, e1});
+    tm.rec.push_back(TimedRec{kind, what, e0, e1});
     e0 = e1 = nullptr;
     return e;
   }
@@ -487,7 +506,7 @@ struct TimedLaunch {
 
 #define ARDIT_TIMED(kind, expr, what)                              \
   do {                                                             \
-    TimedLaunch tl_(st, kind);                                     \
+    TimedLaunch tl_(st, kind, what);                               \
     ARDIT_HIP(tl_.begin(), "hipEventRecord");                      \
     ARDIT_HIP(expr, what);                                         \
     ARDIT_HIP(tl_.end(), "hipEventRecord");                        \
@@ -1293,6 +1312,108 @@ int ardit_timing_collect_kind(int32_t kind, int32_t* launches, double* total_ms)
 
 int ardit_timing_collect(int32_t* launches, double* total_ms) try {
   return ardit_timing_collect_kind(kTimeAttn, launches, total_ms);
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_timing_flush(void* buf, size_t bytes) try {
+  if ((buf == nullptr) != (bytes == 0))
+    return fail(ARDIT_EINVAL, "timing flush: buffer and size must be both set or both empty");
+  if (buf && (misaligned(buf) || bytes % 16 != 0 || bytes < 128 * 1024))
+    return fail(ARDIT_EINVAL, "timing flush buffer must be 16-byte aligned, its size a multiple "
+                "of 16 of at least 128 KiB");
+  Timing& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  // the read covers all but the last 64 KiB, which take the read's
+  // per-workgroup words (at most 32 KiB of them)
+  t.flush = buf;
+  t.flush_bytes = buf ? bytes - 64 * 1024 : 0;
+  t.flush_sink = buf ? reinterpret_cast<uint32_t*>(static_cast<char*>(buf) + t.flush_bytes)
+                     : nullptr;
+  return ARDIT_OK;
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_timing_records(int32_t kind, int32_t max_records, const char** names, double* ms,
+                         int32_t* n_records) try {
+  if (!n_records || (max_records > 0 && (!names || !ms)) || max_records < 0)
+    return fail(ARDIT_EINVAL, "timing records: NULL output or negative room");
+  if (kind < 0 || kind >= kTimeKinds) return fail(ARDIT_EINVAL, "timing kind %d", kind);
+  Timing& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  int32_t n = 0;
+  for (const auto& r : t.rec) n += r.kind == kind;
+  *n_records = n;
+  if (n > max_records)
+    return fail(ARDIT_ECAPACITY, "%d timed launches of kind %d, room for %d", n, kind,
+                max_records);
+  int status = ARDIT_OK;
+  std::vector<TimedRec> keep;
+  int32_t i = 0;
+  for (auto& r : t.rec) {
+    if (r.kind != kind) {
+      keep.push_back(r);
+      continue;
+    }
+    float m = 0.f;
+    hipError_t e = hipEventSynchronize(r.e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&m, r.e0, r.e1);
+    if (e != hipSuccess && status == ARDIT_OK) status = hip_fail(e, "timing events");
+    names[i] = r.what;
+    ms[i] = m;
+    ++i;
+    t.pool.push_back(r.e0);
+    t.pool.push_back(r.e1);
+  }
+  t.rec.swap(keep);
+  return status;
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_micro_mfma(hipStream_t stream, int32_t dtype, int32_t workgroups, int32_t iters,
+                     float* sink, double* flops) try {
+  if (dtype != 0 && dtype != 1) return fail(ARDIT_EINVAL, "micro mfma dtype %d not 0 or 1", dtype);
+  if (workgroups < 1 || workgroups > (1 << 20) || iters < 1)
+    return fail(ARDIT_EINVAL, "micro mfma: workgroups %d, iters %d", workgroups, iters);
+  if (!sink || !flops) return fail(ARDIT_EINVAL, "micro mfma: NULL sink or flops");
+  *flops = static_cast<double>(workgroups) * 4 * iters * micro_mfma_flops_per_wave_iter(dtype);
+  ARDIT_HIP(launch_micro_mfma(stream, dtype, workgroups, iters, sink), "micro mfma launch");
+  return ARDIT_OK;
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_micro_copy(hipStream_t stream, const void* src, void* dst, size_t bytes) try {
+  if (!src || !dst || misaligned(src) || misaligned(dst) || bytes % 16 != 0)
+    return fail(ARDIT_EINVAL, "micro copy: 16-byte aligned buffers and a multiple of 16 bytes");
+  if (overlaps(src, bytes, dst, bytes)) return fail(ARDIT_EINVAL, "micro copy: buffers overlap");
+  ARDIT_HIP(launch_micro_copy(stream, src, dst, bytes), "micro copy launch");
+  return ARDIT_OK;
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_micro_read(hipStream_t stream, const void* src, size_t bytes, void* sink,
+                     size_t sink_bytes) try {
+  if (!src || misaligned(src) || bytes % 16 != 0)
+    return fail(ARDIT_EINVAL, "micro read: a 16-byte aligned buffer and a multiple of 16 bytes");
+  const size_t need = sizeof(uint32_t) * static_cast<size_t>(micro_read_workgroups(bytes));
+  if (!sink || reinterpret_cast<uintptr_t>(sink) % 4 != 0 || sink_bytes < need)
+    return fail(ARDIT_EINVAL, "micro read: a 4-byte aligned sink of at least %zu bytes", need);
+  ARDIT_HIP(launch_micro_read(stream, src, bytes, static_cast<uint32_t*>(sink)),
+            "micro read launch");
+  return ARDIT_OK;
+} catch (...) {
+  return host_failure();
+}
+
+int ardit_micro_fill(hipStream_t stream, void* dst, size_t bytes, uint32_t value) try {
+  if (!dst || misaligned(dst) || bytes % 16 != 0)
+    return fail(ARDIT_EINVAL, "micro fill: a 16-byte aligned buffer and a multiple of 16 bytes");
+  ARDIT_HIP(launch_fill(stream, dst, bytes, value), "micro fill launch");
+  return ARDIT_OK;
 } catch (...) {
   return host_failure();
 }

@@ -219,4 +219,19 @@ struct SamplerArgs {
 hipError_t launch_sampler(hipStream_t st, const bf16_t* x, const bf16_t* v, const bf16_t* eps,
                           bf16_t* out, const SamplerArgs& a);
 
+// ------------------------------------------------------ measurement
+// flops one wave performs per iteration of the MFMA peak kernel
+double micro_mfma_flops_per_wave_iter(int dtype);
+// dtype 0: bf16 (v_mfma_f32_16x16x32_bf16), 1: fp8 e4m3 (v_mfma_scale_f32_32x32x64_f8f6f4);
+// workgroups of 256 threads (4 waves); sink: workgroups * 256 floats
+hipError_t launch_micro_mfma(hipStream_t st, int dtype, int workgroups, int iters, float* sink);
+// dst = src, bytes / 16 chunks of 16 bytes (16-byte aligned)
+hipError_t launch_micro_copy(hipStream_t st, const void* src, void* dst, size_t bytes);
+// reads bytes / 16 chunks of 16 bytes of src, one word per workgroup into sink
+// (micro_read_workgroups(bytes) words)
+int micro_read_workgroups(size_t bytes);
+hipError_t launch_micro_read(hipStream_t st, const void* src, size_t bytes, uint32_t* sink);
+// dst filled with a 32-bit value, bytes / 16 chunks of 16 bytes
+hipError_t launch_fill(hipStream_t st, void* dst, size_t bytes, uint32_t value);
+
 }  // namespace ardit

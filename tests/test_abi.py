@@ -356,3 +356,25 @@ def test_noalloc_attention_host_rejections():
     assert "72" in A.ardit_last_error() or "scratch" in A.ardit_last_error()
     assert _status(A.ardit_attn_fwd_noalloc, FAKE, d, A.Batch([64], [256]), 0,
                    _kv(max_frames=9), FAKE) == -1
+
+
+def test_timing_flush_records_and_micro_host_checks():
+    """Host-side checks of the cold-timing flush, the per-launch records and
+    the measurement kernels (nothing is launched here)."""
+    assert _status(A.ardit_timing_flush, FAKE, 0) == -1          # buffer without size
+    assert _status(A.ardit_timing_flush, None, 64) == -1         # size without buffer
+    assert _status(A.ardit_timing_flush, FAKE + 8, 64) == -1     # misaligned
+    assert _status(A.ardit_timing_flush, FAKE, 24) == -1         # not a multiple of 16
+    A.ardit_timing_flush(FAKE, 1 << 20)
+    A.ardit_timing_flush(None, 0)
+    assert _status(A.ardit_timing_records, 3) == -1
+    assert A.ardit_timing_records(A.TIME_ELEMENTWISE) == []
+    assert _status(A.ardit_micro_mfma, FAKE, 2, 4, 10, FAKE) == -1
+    assert _status(A.ardit_micro_mfma, FAKE, 0, 0, 10, FAKE) == -1
+    assert _status(A.ardit_micro_mfma, FAKE, 0, 4, 10, 0) == -1
+    assert _status(A.ardit_micro_copy, FAKE, FAKE, FAKE + 4096, 20) == -1
+    assert _status(A.ardit_micro_copy, FAKE, FAKE, FAKE + 16, 4096) == -1   # overlap
+    assert _status(A.ardit_micro_fill, FAKE, FAKE + 4, 64) == -1
+    assert _status(A.ardit_micro_read, FAKE, FAKE, 1 << 20, FAKE, 16) == -1   # sink too small
+    assert _status(A.ardit_micro_read, FAKE, FAKE + 8, 1 << 20, FAKE, 1 << 15) == -1
+    assert _status(A.ardit_timing_flush, FAKE, 64 * 1024) == -1             # below 128 KiB
