@@ -29,7 +29,8 @@ int ardit_micro_mfma(hipStream_t stream, int32_t dtype, int32_t workgroups, int3
                      float* sink, double* flops);
 
 /* Device copy: dst = src, `bytes` read and `bytes` written with 16-byte
- * accesses (16-byte aligned, non-overlapping, bytes % 16 == 0). */
+ * streaming (nontemporal) accesses (16-byte aligned, non-overlapping,
+ * bytes % 16 == 0). */
 int ardit_micro_copy(hipStream_t stream, const void* src, void* dst, size_t bytes);
 
 /* Device read of `bytes` of src (16-byte aligned, bytes % 16 == 0) with
