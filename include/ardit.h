@@ -52,8 +52,10 @@
  *    ctx_k / ctx_v, where ctx_off_b is the sum of the earlier streams'
  *    ctx_lens; within a stream keys are [H][L_x][d] and values [H][d][L_x].
  *  - Supported shapes: head_dim in {64, 128}; dim = n_heads * head_dim and
- *    dim, ffn_dim multiples of 128; lat_h * lat_w a multiple of 8; at most
- *    ARDIT_MAX_STREAMS streams per call.
+ *    dim, ffn_dim multiples of 128; T = lat_h * lat_w a multiple of 8 with
+ *    T + gcd(T, 64) >= 64 (a 64-key attention tile spans at most two frame
+ *    pages: T in {8, 16, 24, 40} is rejected); at most ARDIT_MAX_STREAMS
+ *    streams per call.
  */
 #ifndef ARDIT_H
 #define ARDIT_H

@@ -68,6 +68,16 @@ int check_dims(const ardit_dims* d) {
   const int64_t T = static_cast<int64_t>(d->lat_h) * d->lat_w;
   if (T % 8 != 0) return fail(ARDIT_EUNSUPPORTED, "lat_h * lat_w = %lld not a multiple of 8",
                               static_cast<long long>(T));
+  // a 64-key attention tile may span at most two frame pages: tiles start at
+  // multiples of 64, so the furthest one reaches T - gcd(T, 64) + 63 < 2 T
+  {
+    int64_t gcd = 64;
+    while (T % gcd != 0) gcd >>= 1;
+    if (T > 0 && T + gcd < 64)
+      return fail(ARDIT_EUNSUPPORTED,
+                  "lat_h * lat_w = %lld: a 64-key tile would span more than two frames",
+                  static_cast<long long>(T));
+  }
   if (T * d->frames_per_chunk > (1 << 20)) return fail(ARDIT_ESHAPE, "chunk too large");
   if (!(d->eps > 0.f) || !(d->rope_theta > 0.f))
     return fail(ARDIT_EINVAL, "eps and rope_theta must be positive");

@@ -71,6 +71,9 @@ def _block(dims=None, cache_len=384, pos=6, ctx_len=32, kv=None, ws_bytes=None, 
     (dict(dim=320, n_heads=5), -5),                  # D not a multiple of 128
     (dict(ffn_dim=1000), -5),
     (dict(lat_h=3, lat_w=3), -5),                    # T not a multiple of 8
+    (dict(lat_h=3, lat_w=8), -5),                    # T = 24: a 64-key tile spans 4 frames
+    (dict(lat_h=5, lat_w=8), -5),                    # T = 40: 3 frames
+    (dict(lat_h=2, lat_w=8), -5),                    # T = 16
     (dict(lat_w=0), -2),
 ])
 def test_dims_rejected(kw, code):
