@@ -29,13 +29,23 @@ namespace ardit {
 
 namespace {
 
-// 16 bytes per lane from src to LDS at lds + 16 * lane (lds must be the same
-// for all lanes of the wave)
-__device__ __forceinline__ void lds_dma16(const void* src, const void* lds) {
-  const uint32_t m = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
-      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char*)lds)));
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(m) : "m0");
+// 16 bytes per lane from base + off to LDS byte address m0 + 16 * lane.  base
+// and m0 are the same for every lane of the wave and live in scalar
+// registers, so issuing a load costs no vector instruction.
+__device__ __forceinline__ void lds_dma16(const char* base, uint32_t off, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %2"
+               :: "v"(off), "s"(m0), "s"(base) : "m0");
+}
+
+// A pointer the compiler may hold in vector registers, made scalar (it is the
+// same in every lane).  readfirstlane returns int, so each half goes through
+// uint32_t before it is widened: a low half with bit 31 set must not be
+// sign-extended into the high half.
+__device__ __forceinline__ const char* uniform_ptr(const void* p) {
+  const uint64_t b = reinterpret_cast<uint64_t>(p);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+  return reinterpret_cast<const char*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
 constexpr int BM = 128, BN = 256, BK = 64, NT = 512, STAGES = 3;
@@ -108,30 +118,37 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
   const int wm = wave / NWN, wn = wave % NWN;
 
   // Load instruction j of this wave fills the 8 LDS rows 8 (wave * INS + j) .. + 7: lane i
-  // writes slot i % 8 of row 8 (...) + i / 8, which holds chunk (i % 8) ^ swz(row).
-  const char* a_src[A_INS];
-  const char* w_src[W_INS];
+  // writes slot i % 8 of row 8 (...) + i / 8, which holds chunk (i % 8) ^ swz(row).  The
+  // tile's first row (scalar) plus a per-lane byte offset fixed for the whole K loop.
+  const char* a_base = uniform_ptr(A + static_cast<size_t>(tm) * BM * lda);
+  const char* w_base = uniform_ptr(W + static_cast<size_t>(tn) * BN * ldw);
+  uint32_t a_off[A_INS], w_off[W_INS];
 #pragma unroll
   for (int j = 0; j < A_INS; ++j) {
     const int r = 8 * (wave * A_INS + j) + (lane >> 3);
     const int c = (lane & 7) ^ swz(r);
-    a_src[j] = reinterpret_cast<const char*>(A + static_cast<size_t>(min(tm * BM + r, M - 1)) * lda) + c * 16;
+    a_off[j] = static_cast<uint32_t>((min(tm * BM + r, M - 1) - tm * BM) * lda * 2 + c * 16);
   }
 #pragma unroll
   for (int j = 0; j < W_INS; ++j) {
     const int r = 8 * (wave * W_INS + j) + (lane >> 3);
     const int c = (lane & 7) ^ swz(r);
-    w_src[j] = reinterpret_cast<const char*>(W + static_cast<size_t>(min(tn * BN + r, N - 1)) * ldw) + c * 16;
+    w_off[j] = static_cast<uint32_t>((min(tn * BN + r, N - 1) - tn * BN) * ldw * 2 + c * 16);
   }
+  // LDS byte addresses of this wave's first 1 KB blocks of the A and W parts
+  // of stage 0 (the wave index made scalar: it is the same in every lane)
+  const uint32_t wave_s = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave));
+  const uint32_t smem_s = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char*)smem))));
+  const uint32_t lds_a = smem_s + wave_s * (A_INS * 1024u);
+  const uint32_t lds_w = smem_s + A_BYTES + wave_s * (W_INS * 1024u);
   auto issue = [&](int kt) {
-    unsigned char* st = smem + (kt % STAGES) * STAGE_BYTES;
+    const uint32_t so = static_cast<uint32_t>((kt % STAGES) * STAGE_BYTES);
     const int koff = kt * ROW_BYTES;
 #pragma unroll
-    for (int j = 0; j < A_INS; ++j)
-      lds_dma16(a_src[j] + koff, st + (wave * A_INS + j) * 1024);
+    for (int j = 0; j < A_INS; ++j) lds_dma16(a_base + koff, a_off[j], lds_a + so + 1024u * j);
 #pragma unroll
-    for (int j = 0; j < W_INS; ++j)
-      lds_dma16(w_src[j] + koff, st + A_BYTES + (wave * W_INS + j) * 1024);
+    for (int j = 0; j < W_INS; ++j) lds_dma16(w_base + koff, w_off[j], lds_w + so + 1024u * j);
   };
 
   f32x4 acc[MB][NB];
