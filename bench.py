@@ -95,6 +95,9 @@ def parse():
     p.add_argument("--micro", action="store_true",
                    help="only run the measurement kernels: MFMA throughput (bf16, fp8) and "
                         "the HBM copy, and print one line with the measured peaks")
+    p.add_argument("--sp2", action="store_true",
+                   help="time one GPU's share of Ulysses SP2: every query of the chunk for half "
+                        "the heads over the full keys (paged self-attention alone)")
     p.add_argument("--cold", action="store_true",
                    help="with --workload ragged: time every elementwise launch of one step "
                         "after a 512 MiB write (cold caches) and warm, per kernel")
@@ -209,6 +212,70 @@ def micro_main():
               "published": {"mfma_bf16_tflops": PEAK_BF16_TFLOPS, "mfma_fp8_tflops": PEAK_FP8_TFLOPS,
                             "hbm_tbps": 8.0}})
     print(json.dumps(m), flush=True)
+
+
+def sp2_share_shape(sh):
+    """The block shape one GPU sees under Ulysses SP2 (Appendix C): after the
+    all-to-all it holds every token of the chunk for half the heads, and the
+    head-partitioned pages hold those heads only."""
+    from workloads import BlockShape
+    hs = sh.n_heads // 2
+    return BlockShape(dim=hs * sh.head_dim, n_heads=hs, head_dim=sh.head_dim, ffn_dim=sh.ffn_dim,
+                      frames=sh.frames, lat_h=sh.lat_h, lat_w=sh.lat_w, eps=sh.eps,
+                      theta=sh.theta, time_freq_dim=sh.time_freq_dim)
+
+
+def sp2_main(args):
+    """One GPU's share of Ulysses SP2: 4680 queries of half the heads over the
+    stream's full key length through its (head-partitioned) pages; the paged
+    self-attention launch timed alone with the library's events."""
+    import torch
+    from paper_2606_15319_amd import ardit as A
+    from workloads import WORKLOADS, stream_page_ids
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = WORKLOADS[args.workload]
+    sh = sp2_share_shape(wl.shape)
+    H, d, T, L = sh.n_heads, sh.head_dim, sh.tokens_per_frame, sh.chunk_tokens
+    cache = wl.cache_chunks[0] * L
+    ids, n_pages = stream_page_ids(wl)
+    ids = ids[:1]
+    g = torch.Generator(device=dev)
+    g.manual_seed(15319 + wl.wid)
+    kp = torch.randn((n_pages, H, T, d), generator=g, device=dev).to(torch.bfloat16)
+    vp = torch.randn((n_pages, H, d, T), generator=g, device=dev).to(torch.bfloat16)
+    q = torch.randn((L, H * d), generator=g, device=dev).to(torch.bfloat16)
+    o = torch.empty_like(q)
+    table = torch.tensor([ids[0]], dtype=torch.int32, device=dev)
+    kv = A.kv_paged(kp, vp, table, n_pages, len(ids[0]))
+    dims = A.dims_from_shape(sh)
+    batch = A.Batch([L], [cache])
+    nws = A.ardit_workspace_size(dims, batch)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    for _ in range(max(args.warmup, 1)):
+        A.ardit_attn_fwd(None, dims, batch, q, kv, o, ws, nws)
+    torch.cuda.synchronize()
+    A.ardit_timing_collect()
+    A.ardit_timing_enable(True)
+    for _ in range(args.steps):
+        A.ardit_attn_fwd(None, dims, batch, q, kv, o, ws, nws)
+    torch.cuda.synchronize()
+    A.ardit_timing_enable(False)
+    n, ms = A.ardit_timing_collect()
+    avg = ms / max(n, 1)
+    L_k = cache + L
+    flops = 4.0 * L * L_k * H * d
+    items = H * ((L + 255) // 256)
+    meas = measured_peaks(A)
+    tf = flops / (avg * 1e-3) / 1e12
+    print(json.dumps({
+        "probe": "one GPU's share of Ulysses SP2",
+        "workload": f"{wl.name}: {H} of {wl.shape.n_heads} heads of {d}, {L} queries over {L_k} "
+                    f"keys through the stream's pages", "items": items,
+        "split_schedule": items * 4 < 3 * 256,
+        "ms_per_launch": round(avg, 4), "launches": n, "gflop": round(flops / 1e9, 1),
+        "tflops": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+        "frac_of_measured": round(tf / meas["mfma_bf16_tflops"], 4)}), flush=True)
 
 
 # bytes each elementwise launch of a block moves per token row and hidden
@@ -484,6 +551,12 @@ def main():
         return
     if args.micro:
         micro_main()
+        return
+    if args.sp2:
+        if args.workload not in ("large", "block13b"):
+            print("--sp2 takes the large or block13b workload", file=sys.stderr)
+            sys.exit(2)
+        sp2_main(args)
         return
     if args.cold and args.workload != "ragged":
         print("--cold times the elementwise kernels of the ragged workload only", file=sys.stderr)

@@ -315,6 +315,41 @@ def test_attn_chunk_over_cache_4680x14040(A):
     parity(host_f32(o)[rows], ref, "attn 4680x14040")
 
 
+@pytest.mark.parametrize("name", ["block13b", "large"])
+def test_attn_sp2_share_full_keys(A, name):
+    """One GPU's share of Ulysses SP2 (Appendix C): after the all-to-all a GPU
+    holds every query of the chunk for half the heads and attends over the
+    head-partitioned pages at the full key length -- the 1.3B-class block's 6
+    of 12 heads over 32760 keys (114 items, so the split schedule and its
+    merge run at full length) and the large block's 20 of 40 heads over 37440
+    keys through its wrapped ring.  Q and K RMS-normalised over the share's
+    width, V ~ N(0, 1); sampled query rows against the oracle."""
+    import torch
+    from workloads import stream_page_ids
+    wl = WORKLOADS[name]
+    full = wl.shape
+    hs = full.n_heads // 2
+    sh = BlockShape(dim=hs * full.head_dim, n_heads=hs, head_dim=full.head_dim,
+                    ffn_dim=full.ffn_dim, frames=full.frames, lat_h=full.lat_h, lat_w=full.lat_w)
+    H, d, D, L = sh.n_heads, sh.head_dim, sh.dim, sh.chunk_tokens
+    cache = wl.cache_chunks[0] * L
+    rng = make_rng(60 + wl.wid)
+    q = bf16_round(O.rms_norm(rng.standard_normal((L, D), dtype=np.float32), sh.eps))
+    k = bf16_round(O.rms_norm(rng.standard_normal((cache + L, D), dtype=np.float32), sh.eps))
+    v = normal_bf16(rng, (cache + L, H, d))
+    ids, n_pages = stream_page_ids(wl)
+    pc = PagedCache(sh, ids[:1], n_pages)
+    pc.fill_stream(0, k.reshape(-1, H, d), v)
+    pc.upload()
+    qd = dev_bf16(q)
+    o = torch.empty_like(qd)
+    _attn(A, A.dims_from_shape(sh), A.Batch([L], [cache]), qd, pc.kv(A), o)
+    _sync()
+    rows = sample_rows(L, seed=3)
+    ref = O.attention(q[rows].reshape(-1, H, d), k.reshape(-1, H, d), v).reshape(len(rows), D)
+    parity(host_f32(o)[rows], ref, f"SP2 share {name}", quantum=ref)
+
+
 # -------------------------------------------------------------------- block
 def _check_block(run, b, rows=None, tag=""):
     ref = run.reference(b, rows=rows)
