@@ -23,6 +23,8 @@
 // 16-byte stores after applying bias / GELU / gate * y + residual in fp32.
 // Rows past M read a clamped row and store nothing; an N ending on a
 // half tile (N % 256 == 128) clamps W rows the same way.
+#include <type_traits>
+
 #include "launch.h"
 
 namespace ardit {
@@ -207,10 +209,12 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
   __syncthreads();
   bf16x8 fa0[MB], fw0[NB], fa1[MB], fw1[NB];
   read_half(smem, 0, fa0, fw0);
-  for (int kt = 0; kt < nk; ++kt) {
+  // one K step on stage S (a constant: the loop runs the three stages in
+  // turn, so every LDS address is a register plus an immediate)
+  auto step = [&](int kt, auto s_c) __attribute__((always_inline)) {
+    constexpr int S = decltype(s_c)::value;
     if (kt + 2 < nk) issue(kt + 2);
-    const unsigned char* st = smem + (kt % STAGES) * STAGE_BYTES;
-    read_half(st, 1, fa1, fw1);
+    read_half(smem + S * STAGE_BYTES, 1, fa1, fw1);
     mma(fa0, fw0);
     interleave();
     if (kt + 1 < nk) {
@@ -220,10 +224,16 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
         asm volatile("s_waitcnt vmcnt(0)");
       }
       __syncthreads();
-      read_half(smem + ((kt + 1) % STAGES) * STAGE_BYTES, 0, fa0, fw0);
+      read_half(smem + ((S + 1) % STAGES) * STAGE_BYTES, 0, fa0, fw0);
     }
     mma(fa1, fw1);
     interleave();
+  };
+  static_assert(STAGES == 3, "the K loop is unrolled over three stages");
+  for (int kt = 0; kt < nk; kt += STAGES) {
+    step(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 < nk) step(kt + 1, std::integral_constant<int, 1>{});
+    if (kt + 2 < nk) step(kt + 2, std::integral_constant<int, 2>{});
   }
 
   // epilogue: lane owns row m and columns n0..n0+3 of each (mb, nb)
