@@ -644,6 +644,39 @@ def test_fp8_weight_quantisation_within_bound():
         assert 1e-3 < rel < 0.1
 
 
+@pytest.mark.parametrize("n_keys", [32760, 37440])
+def test_dense_attention_bar_rejects_wrong_outputs(n_keys):
+    """The bar the full-size self-attention checks use (harness.parity: max
+    error 2e-2 of the RMS plus half a bf16 ulp, cosine 0.9995; and the looser
+    5e-2 against the block's own o) at the 1.3B-class and large key lengths:
+    the bf16-rounded exact output passes, while an all-zero output, half the
+    output, and the output with one key's value missing (the attention over
+    all keys but the largest-weight one of each row) fail."""
+    from harness import parity
+    from workloads import bf16_round
+    rng = np.random.default_rng(71 + n_keys % 11)
+    H, d, R = 2, 128, 16
+    q = O.rms_norm(rng.standard_normal((R, H * d)), 1e-6).reshape(R, H, d)
+    k = O.rms_norm(rng.standard_normal((n_keys, H * d)), 1e-6).reshape(n_keys, H, d)
+    v = rng.standard_normal((n_keys, H, d))
+    o = O.attention(q, k, v).reshape(R, H * d)
+    parity(bf16_round(o), o, "exact", quantum=o)
+    # drop, per row and head, the key of largest weight
+    s = np.einsum("rhd,khd->rhk", q, k) / math.sqrt(d)
+    top = s.argmax(axis=2)
+    o_drop = np.empty((R, H, d))
+    for r in range(R):
+        for h in range(H):
+            keep = np.ones(n_keys, bool)
+            keep[top[r, h]] = False
+            o_drop[r, h] = O.attention(q[r:r + 1, h:h + 1], k[keep][:, h:h + 1], v[keep][:, h:h + 1])[0, 0]
+    for bad, tag in ((np.zeros_like(o), "zero"), (0.5 * o, "half"),
+                     (o_drop.reshape(R, H * d), "largest key dropped")):
+        for tol in (2e-2, 5e-2):
+            with pytest.raises(AssertionError):
+                parity(bad, o, tag, tol=tol, quantum=o)
+
+
 @pytest.mark.parametrize("n_keys", [14040, 32760])
 def test_fp8_statistical_criterion_discriminates(n_keys):
     """The FP8 parity criterion (harness.fp8_parity) at the attention
