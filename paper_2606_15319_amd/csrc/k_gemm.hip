@@ -19,8 +19,9 @@
 //
 // The MFMA computes C^T = W A^T: W rows feed the A operand and A rows the B
 // operand, so each lane ends up owning one output row m and four
-// consecutive columns n per block, which the epilogue writes as 8- or
-// 16-byte stores after applying bias / GELU / gate * y + residual in fp32.
+// consecutive columns n per block.  The epilogue applies bias / GELU /
+// gate * y + residual in fp32, staging the tile through LDS so that the
+// residual is read and C written one contiguous row at a time.
 // Rows past M read a clamped row and store nothing; an N ending on a
 // half tile (N % 256 == 128) clamps W rows the same way.
 #include <type_traits>
@@ -236,39 +237,78 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
     if (kt + 2 < nk) step(kt + 2, std::integral_constant<int, 2>{});
   }
 
-  // epilogue: lane owns row m and columns n0..n0+3 of each (mb, nb)
-  if (tn * BN + WN * wn >= N) return;
+  // epilogue through LDS (free once every wave has read its last fragments):
+  // each lane writes y = acc + bias (GELU applied) for its row and four
+  // columns of every block into a row-major fp32 tile, and the workgroup
+  // then walks the tile one row per wave, each lane taking four consecutive
+  // columns, so the residual is read and C written as whole contiguous rows.
+  // The loads of four rows are issued before any of them is used, so the
+  // epilogue waits on memory four times per wave rather than once per row.
+  // Rows are padded by 16 bytes: the 16 lanes of one write then cover all 64
+  // banks.
+  constexpr int CROW = BN * 4 + 16;
+  constexpr int RB = 4;                               // rows in flight per wave
+  static_assert(BM * CROW <= STAGES * STAGE_BYTES, "C tile in LDS");
+  static_assert(BM % (NWAVES * RB) == 0, "row batches");
+  const bool cols_in = tn * BN + WN * wn < N;   // (a tile may end on a half tile)
+  float bias[NB][4];
+  if (cols_in) {
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int m = tm * BM + WM * wm + 16 * mb + l16;
-    if (m >= M) continue;
-    const int sidx = (EPI == kEpiBiasGateRes) ? m / ep.rows_per_stream : 0;
+    for (int nb = 0; nb < NB; ++nb) load4(ep.bias + tn * BN + WN * wn + 16 * nb + 4 * g, bias[nb]);
+  }
+  __syncthreads();
+  if (cols_in) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int n0 = tn * BN + WN * wn + 16 * nb + 4 * g;
-      float y[4], bias[4];
-      load4(ep.bias + n0, bias);
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = WM * wm + 16 * mb + l16;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = acc[mb][nb][e] + bias[e];
-      if (EPI == kEpiBiasGelu) {
+      for (int nb = 0; nb < NB; ++nb) {
+        const int cl = WN * wn + 16 * nb + 4 * g;
+        float y[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) y[e] = gelu_tanh(y[e]);
-      }
-      if (EPI == kEpiBiasGateRes || EPI == kEpiBiasRes) {
-        float res[4];
-        load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res);
-        if (EPI == kEpiBiasGateRes) {
-          float gm4[4], gt4[4];
-          load4(ep.mod + (static_cast<size_t>(sidx) * 6 + ep.gate_row) * ep.dim + n0, gm4);
-          load4(ep.mod_table + static_cast<size_t>(ep.gate_row) * ep.dim + n0, gt4);
+        for (int e = 0; e < 4; ++e) y[e] = acc[mb][nb][e] + bias[nb][e];
+        if (EPI == kEpiBiasGelu) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) y[e] = res[e] + (gm4[e] + gt4[e]) * y[e];
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) y[e] = res[e] + y[e];
+          for (int e = 0; e < 4; ++e) y[e] = gelu_tanh(y[e]);
         }
+        *reinterpret_cast<float4*>(smem + r * CROW + cl * 4) = make_float4(y[0], y[1], y[2], y[3]);
       }
-      store4(C + static_cast<size_t>(m) * ldc + n0, y);
+    }
+  }
+  __syncthreads();
+  const int cl = 4 * lane;
+  const int n0 = tn * BN + cl;
+  if (n0 >= N) return;
+  float gt4[4] = {0.f, 0.f, 0.f, 0.f};
+  if (EPI == kEpiBiasGateRes) load4(ep.mod_table + static_cast<size_t>(ep.gate_row) * ep.dim + n0, gt4);
+#pragma unroll
+  for (int b = 0; b < BM / (NWAVES * RB); ++b) {
+    float res[RB][4], gm[RB][4];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int m = min(tm * BM + wave + NWAVES * (RB * b + i), M - 1);
+      if (EPI == kEpiBiasGateRes || EPI == kEpiBiasRes)
+        load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res[i]);
+      if (EPI == kEpiBiasGateRes)
+        load4(ep.mod + (static_cast<size_t>(m / ep.rows_per_stream) * 6 + ep.gate_row) * ep.dim + n0,
+              gm[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int rr = wave + NWAVES * (RB * b + i);
+      const int m = tm * BM + rr;
+      if (m < M) {
+        const float4 t = *reinterpret_cast<const float4*>(smem + rr * CROW + cl * 4);
+        float y[4] = {t.x, t.y, t.z, t.w};
+        if (EPI == kEpiBiasGateRes) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = res[i][e] + (gm[i][e] + gt4[e]) * y[e];
+        } else if (EPI == kEpiBiasRes) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = res[i][e] + y[e];
+        }
+        store4(C + static_cast<size_t>(m) * ldc + n0, y);
+      }
     }
   }
 }
