@@ -242,15 +242,35 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
   // columns of every block into a row-major fp32 tile, and the workgroup
   // then walks the tile one row per wave, each lane taking four consecutive
   // columns, so the residual is read and C written as whole contiguous rows.
-  // The loads of four rows are issued before any of them is used, so the
-  // epilogue waits on memory four times per wave rather than once per row.
+  // The residual and gate loads of a wave's rows go out in two batches of
+  // eight, the first before the tile is staged and the second before the
+  // first is used, so their latency hides behind the staging and the stores.
   // Rows are padded by 16 bytes: the 16 lanes of one write then cover all 64
   // banks.
   constexpr int CROW = BN * 4 + 16;
-  constexpr int RB = 4;                               // rows in flight per wave
+  constexpr int RB = 8;                               // rows per batch and wave
+  constexpr int NBATCH = BM / (NWAVES * RB);
   static_assert(BM * CROW <= STAGES * STAGE_BYTES, "C tile in LDS");
-  static_assert(BM % (NWAVES * RB) == 0, "row batches");
+  static_assert(BM % (NWAVES * RB) == 0 && NBATCH == 2, "row batches");
+  constexpr bool HAS_RES = EPI == kEpiBiasGateRes || EPI == kEpiBiasRes;
   const bool cols_in = tn * BN + WN * wn < N;   // (a tile may end on a half tile)
+  const int cl = 4 * lane;
+  const int n0 = min(tn * BN + cl, N - 4);      // lanes past N load a valid column, store nothing
+  float res[NBATCH][RB][4], gmod[NBATCH][RB][4];
+  auto load_batch = [&](int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int m = min(tm * BM + wave + NWAVES * (RB * b + i), M - 1);
+      if (HAS_RES)
+        load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res[b][i]);
+      if (EPI == kEpiBiasGateRes)
+        load4(ep.mod + (static_cast<size_t>(m / ep.rows_per_stream) * 6 + ep.gate_row) * ep.dim + n0,
+              gmod[b][i]);
+    }
+  };
+  float gt4[4] = {0.f, 0.f, 0.f, 0.f};
+  if (EPI == kEpiBiasGateRes) load4(ep.mod_table + static_cast<size_t>(ep.gate_row) * ep.dim + n0, gt4);
+  load_batch(0);
   float bias[NB][4];
   if (cols_in) {
 #pragma unroll
@@ -263,7 +283,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
       const int r = WM * wm + 16 * mb + l16;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const int cl = WN * wn + 16 * nb + 4 * g;
+        const int c = WN * wn + 16 * nb + 4 * g;
         float y[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) y[e] = acc[mb][nb][e] + bias[nb][e];
@@ -271,28 +291,15 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
 #pragma unroll
           for (int e = 0; e < 4; ++e) y[e] = gelu_tanh(y[e]);
         }
-        *reinterpret_cast<float4*>(smem + r * CROW + cl * 4) = make_float4(y[0], y[1], y[2], y[3]);
+        *reinterpret_cast<float4*>(smem + r * CROW + c * 4) = make_float4(y[0], y[1], y[2], y[3]);
       }
     }
   }
   __syncthreads();
-  const int cl = 4 * lane;
-  const int n0 = tn * BN + cl;
-  if (n0 >= N) return;
-  float gt4[4] = {0.f, 0.f, 0.f, 0.f};
-  if (EPI == kEpiBiasGateRes) load4(ep.mod_table + static_cast<size_t>(ep.gate_row) * ep.dim + n0, gt4);
+  load_batch(1);
+  if (tn * BN + cl >= N) return;
 #pragma unroll
-  for (int b = 0; b < BM / (NWAVES * RB); ++b) {
-    float res[RB][4], gm[RB][4];
-#pragma unroll
-    for (int i = 0; i < RB; ++i) {
-      const int m = min(tm * BM + wave + NWAVES * (RB * b + i), M - 1);
-      if (EPI == kEpiBiasGateRes || EPI == kEpiBiasRes)
-        load4(static_cast<const ResT*>(ep.res) + static_cast<size_t>(m) * ep.ldr + n0, res[i]);
-      if (EPI == kEpiBiasGateRes)
-        load4(ep.mod + (static_cast<size_t>(m / ep.rows_per_stream) * 6 + ep.gate_row) * ep.dim + n0,
-              gm[i]);
-    }
+  for (int b = 0; b < NBATCH; ++b) {
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const int rr = wave + NWAVES * (RB * b + i);
@@ -302,10 +309,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(const bf16_t* __restrict__ 
         float y[4] = {t.x, t.y, t.z, t.w};
         if (EPI == kEpiBiasGateRes) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) y[e] = res[i][e] + (gm[i][e] + gt4[e]) * y[e];
+          for (int e = 0; e < 4; ++e) y[e] = res[b][i][e] + (gmod[b][i][e] + gt4[e]) * y[e];
         } else if (EPI == kEpiBiasRes) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) y[e] = res[i][e] + y[e];
+          for (int e = 0; e < 4; ++e) y[e] = res[b][i][e] + y[e];
         }
         store4(C + static_cast<size_t>(m) * ldc + n0, y);
       }
