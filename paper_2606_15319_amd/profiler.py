@@ -17,12 +17,6 @@ FP16) on the same starting noise, weights and cache -- how far the
 configuration moves the output, not how good it looks.
 
 Run: python -m paper_2606_15319_amd.profiler --out result.json [--md summary.md]
-
---controller PROFILE times the host controller instead (no GPU): one
-ardit_control_tick over the frontier of a profile written by the run above
-(its JSON, or the table of its markdown summary),
-for 64 to 4096 streams with random slack on 16 or 64 workers (the paper
-measures its controller's latency against the stream count, Appendix D.1).
 """
 from __future__ import annotations
 
