@@ -589,6 +589,23 @@ def test_stack_equals_repeated_blocks_and_tracks_oracle(A):
     parity(host_f32(out), x, "30-layer stack", quantum=x, half_ulps=2.0 * np.sqrt(n_layers))
 
 
+def test_block_192_row_gemm_tiles(A):
+    """A 4680-row chunk whose QKV and FFN-up widths (3 * 1152 = 3456) are
+    multiples of 128 but not of 256: the GEMMs take 192-row tiles there (25
+    row tiles, the last holding 72 rows, and a half tile of columns), and
+    128-row tiles for the 1152-wide products; checked against the oracle on
+    sampled rows of two streams."""
+    import dataclasses
+    sh = BlockShape(dim=1152, n_heads=9, head_dim=128, ffn_dim=3456, frames=3, lat_h=30, lat_w=52)
+    wl = dataclasses.replace(WORKLOADS["tiny"], shape=sh, cache_chunks=(1, 0),
+                             frame_pos0=(3, 0), timesteps=(750, 1000), ctx_len=64)
+    run = BlockRun(wl, A, shuffle_pages_seed=11)
+    run.run()
+    _sync()
+    for b in range(2):
+        _check_block(run, b, rows=sample_rows(sh.chunk_tokens, seed=20 + b), tag="gemm-192")
+
+
 @pytest.mark.parametrize("name", ["block13b", "ragged", "large"])
 def test_block_full_size_sampled_rows(A, name):
     """Full-size block step (one layer) of the 1.3B-class, ragged 8-stream and
