@@ -28,7 +28,10 @@ __device__ __forceinline__ void load8(const float* p, float* f) {
   f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
 }
 
-// A workgroup of 4 waves handles kRowsPerGroup consecutive rows, 2 per wave;
+// A workgroup handles kRowsPerGroup consecutive rows: 4 waves of 2 rows, or,
+// for rows of more than 3072 elements, 8 waves of one row each (half the
+// registers per wave, so twice the waves in flight: 17% less time for the
+// norms of 5120-wide rows);
 // the per-row vectors it shares (modulation, gains) are staged once in LDS as
 // fp32, the first four of each 8-element chunk in one array and the last four
 // in a second, so a wave's 16-byte reads are consecutive (pairs of 16-byte
@@ -36,17 +39,22 @@ __device__ __forceinline__ void load8(const float* p, float* f) {
 // its rows, so every row is read from HBM once and all its loads are in
 // flight together.
 constexpr int kRowsPerGroup = 8;
-constexpr int kRowsPerWave = kRowsPerGroup / 4;
+// rows per wave and threads per workgroup for rows of up to 512 MAXC elements
+template <int MAXC> struct RowCfg {
+  static constexpr int RPW = MAXC >= 8 ? 1 : 2;
+  static constexpr int THREADS = 64 * kRowsPerGroup / RPW;
+};
 
 // y = rms(x) * (1 + scale) + shift with scale = mod[b][scale_row] +
 // mod_table[scale_row] and shift likewise.  Streams hold rows_per_stream
 // rows, a multiple of kRowsPerGroup, so a workgroup's rows share one stream.
 template <typename T, int MAXC>
-__global__ __launch_bounds__(256) void adaln_norm_kernel(
+__global__ __launch_bounds__(512) void adaln_norm_kernel(
     const T* __restrict__ x, bf16_t* __restrict__ out, int N, int D,
     const float* __restrict__ mod, const float* __restrict__ mod_table, int shift_row,
     int scale_row, int rows_per_stream, float eps) {
   extern __shared__ float4 lds_mod[];   // D / 4 of (1 + scale), then D / 4 of shift (split halves)
+  constexpr int kRowsPerWave = RowCfg<MAXC>::RPW, NTHR = RowCfg<MAXC>::THREADS;
   const int lane = threadIdx.x & 63;
   const int row0 = blockIdx.x * kRowsPerGroup + (threadIdx.x >> 6) * kRowsPerWave;
   const int nchunk = D >> 3;
@@ -67,7 +75,7 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
     const float4* msc = reinterpret_cast<const float4*>(mod + (static_cast<size_t>(b) * 6 + scale_row) * D);
     const float4* tsh = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(shift_row) * D);
     const float4* tsc = reinterpret_cast<const float4*>(mod_table + static_cast<size_t>(scale_row) * D);
-    for (int k = threadIdx.x; k < D / 8; k += 256) {   // chunk k, both halves
+    for (int k = threadIdx.x; k < D / 8; k += NTHR) {   // chunk k, both halves
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         const float4 a = msc[2 * k + hf], c = tsc[2 * k + hf];
@@ -112,10 +120,11 @@ __global__ __launch_bounds__(256) void adaln_norm_kernel(
 
 // y = rms(x) * gain, the gain staged in LDS as fp32.
 template <typename T, int MAXC>
-__global__ __launch_bounds__(256) void rms_gain_kernel(const T* in, bf16_t* out, int N, int D,
+__global__ __launch_bounds__(512) void rms_gain_kernel(const T* in, bf16_t* out, int N, int D,
                                                         const bf16_t* __restrict__ gain,
                                                         float eps) {
   extern __shared__ float4 lds_gain[];   // D / 4
+  constexpr int kRowsPerWave = RowCfg<MAXC>::RPW, NTHR = RowCfg<MAXC>::THREADS;
   const int lane = threadIdx.x & 63;
   const int row0 = blockIdx.x * kRowsPerGroup + (threadIdx.x >> 6) * kRowsPerWave;
   const int nchunk = D >> 3;
@@ -129,7 +138,7 @@ __global__ __launch_bounds__(256) void rms_gain_kernel(const T* in, bf16_t* out,
       if (c < nchunk) load8(xr + 8 * c, v[r][i]);
     }
   }
-  for (int k = threadIdx.x; k < D / 8; k += 256) {
+  for (int k = threadIdx.x; k < D / 8; k += NTHR) {
     float g[8];
     load8(gain + 8 * k, g);
     lds_gain[k] = make_float4(g[0], g[1], g[2], g[3]);
@@ -175,7 +184,7 @@ static int row_chunks(int D) {
 }
 
 #define ARDIT_ROW_CASE(KERNEL, T, C, LDS, ...) \
-  case C: hipLaunchKernelGGL((KERNEL<T, C>), grid, dim3(256), LDS, st, __VA_ARGS__); break;
+  case C: hipLaunchKernelGGL((KERNEL<T, C>), grid, dim3(RowCfg<C>::THREADS), LDS, st, __VA_ARGS__); break;
 #define ARDIT_ROW_DISPATCH(KERNEL, T, LDS, ...)         \
   switch (row_chunks(D)) {                              \
     ARDIT_ROW_CASE(KERNEL, T, 1, LDS, __VA_ARGS__)      \
@@ -187,7 +196,7 @@ static int row_chunks(int D) {
     ARDIT_ROW_CASE(KERNEL, T, 8, LDS, __VA_ARGS__)      \
     ARDIT_ROW_CASE(KERNEL, T, 10, LDS, __VA_ARGS__)     \
     ARDIT_ROW_CASE(KERNEL, T, 12, LDS, __VA_ARGS__)     \
-    default: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(256), LDS, st, __VA_ARGS__); break; \
+    default: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(RowCfg<16>::THREADS), LDS, st, __VA_ARGS__); break; \
   }
 
 hipError_t launch_adaln_norm(hipStream_t st, const void* x, bool x_f32, bf16_t* out, int N, int D,
@@ -254,13 +263,14 @@ __device__ __forceinline__ int write_page(int p, int n_pages) {
   return p >= 0 && p < n_pages ? p : -1;
 }
 
-// A workgroup handles kRowsPerGroup rows, 2 per wave.  Per row, lane k < d/2
+// A workgroup handles kRowsPerGroup rows (RowCfg: 2 or 1 per wave).  Per row, lane k < d/2
 // computes the rotation (cos, sin) of pair k, shared through LDS; the gains
 // are staged in LDS as fp32; both rows' q and k are loaded before any math.
 // lds_qk: g_q (D / 4 float4), g_k (D / 4), then cos / sin per row
 template <int MAXC>
 __device__ __forceinline__ void qk_norm_rope_group(const QkRopeParams& p, int group,
                                                    float4* lds_qk) {
+  constexpr int kRowsPerWave = RowCfg<MAXC>::RPW, NTHR = RowCfg<MAXC>::THREADS;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int row0 = group * kRowsPerGroup + wave * kRowsPerWave;
@@ -285,7 +295,7 @@ __device__ __forceinline__ void qk_norm_rope_group(const QkRopeParams& p, int gr
       }
     }
   }
-  for (int k = threadIdx.x; k < p.D / 8; k += 256) {
+  for (int k = threadIdx.x; k < p.D / 8; k += NTHR) {
     float g[8];
     unpack8(reinterpret_cast<const uint4*>(p.g_q)[k], g);
     lg_q[k] = make_float4(g[0], g[1], g[2], g[3]);
@@ -386,7 +396,7 @@ __device__ __forceinline__ void qk_norm_rope_group(const QkRopeParams& p, int gr
 }
 
 template <int MAXC>
-__global__ __launch_bounds__(256) void qk_norm_rope_kernel(const QkRopeParams p) {
+__global__ __launch_bounds__(512) void qk_norm_rope_kernel(const QkRopeParams p) {
   extern __shared__ float4 lds_qk[];
   qk_norm_rope_group<MAXC>(p, blockIdx.x, lds_qk);
 }
@@ -440,11 +450,11 @@ hipError_t launch_qk_norm_rope(hipStream_t st, const bf16_t* qkv, int N, const R
   const size_t lds = qk_lds_bytes(g.D);
   switch (row_chunks(g.D)) {
 #define ARDIT_QK_CASE(C) \
-    case C: hipLaunchKernelGGL(qk_norm_rope_kernel<C>, grid, dim3(256), lds, st, p); break;
+    case C: hipLaunchKernelGGL(qk_norm_rope_kernel<C>, grid, dim3(RowCfg<C>::THREADS), lds, st, p); break;
     ARDIT_QK_CASE(1) ARDIT_QK_CASE(2) ARDIT_QK_CASE(3) ARDIT_QK_CASE(4) ARDIT_QK_CASE(5)
     ARDIT_QK_CASE(6) ARDIT_QK_CASE(8) ARDIT_QK_CASE(10) ARDIT_QK_CASE(12)
 #undef ARDIT_QK_CASE
-    default: hipLaunchKernelGGL(qk_norm_rope_kernel<16>, grid, dim3(256), lds, st, p); break;
+    default: hipLaunchKernelGGL(qk_norm_rope_kernel<16>, grid, dim3(RowCfg<16>::THREADS), lds, st, p); break;
   }
   return hipGetLastError();
 }
